@@ -1,0 +1,3 @@
+"""Seeded synthetic inputs shared by the oracle tests, the GPU tests and the benchmark."""
+from .gen import *  # noqa: F401,F403
+from .gen import random_scores  # noqa: F401

@@ -1,0 +1,216 @@
+/*
+ * oasis.h -- C ABI of the OasisKV decode-time hot path on AMD Instinct MI355X (gfx950).
+ *
+ * Paper: "OasisKV: Scaling In-Decode KV Cache Beyond HBM with Lookahead Sparse
+ * Prefetching" (arXiv 2608.08097). One decode step of one layer is
+ *
+ *   oasis_score_blocks       rank every KV block from the draft queries     (paper §4.2.1)
+ *   oasis_select_topk        keep the K best blocks per (request, KV head)   (§4.2.1, §4.2.2, §5.2)
+ *   oasis_stage_blocks       delta-select and gather them from pinned host   (§4.2.3, §4.3, §5.1)
+ *   oasis_sparse_decode_attn attention of the stacked queries over them      (§4.2.1, §4.3, §5.2)
+ *
+ * plus oasis_build_summaries, which makes the compressed keys the scorer reads
+ * (§4.2.1, "Look-ahead attention" figure) once per completed block.
+ *
+ * General conventions
+ * -------------------
+ * - Every pointer is owned by the caller. The library allocates no memory; the
+ *   scratch that a call needs is a caller-provided workspace whose size comes
+ *   from the matching *_workspace_bytes function.
+ * - Calls are asynchronous on `stream` (a hipStream_t passed as void*, NULL =
+ *   the null stream). They return once the kernels are enqueued.
+ * - Host-side checks (null pointers, supported sizes, workspace size) return
+ *   OASIS_ERR_INVALID_ARG or OASIS_ERR_UNSUPPORTED and launch nothing.
+ *   oasis_last_error() then describes the problem (thread-local string).
+ * - A failed kernel launch returns OASIS_ERR_HIP. A fault inside a kernel is
+ *   reported by HIP at the caller's next synchronisation.
+ * - Values that live on the device (context lengths, counts, block ids, page
+ *   ids) are clamped or skipped by the kernels, never trusted for addressing:
+ *   ctx_len is clamped to [0, max_blocks * block_size]; a page id outside
+ *   [0, num_pages) is not read; a selection count is clamped to [0, k].
+ * - No C++ exception crosses this interface.
+ * - bf16 tensors are raw bfloat16 bit patterns (uint16_t).
+ *
+ * Notation: R requests, Hq query heads, Hkv KV heads, G = Hq / Hkv query heads
+ * per KV head (query head qh belongs to KV head qh / G), d = head_dim = 128,
+ * B = block_size, T = num_q_tokens query rows per head (row 0 is the token
+ * being verified, the following rows are draft / lookahead tokens),
+ * NBmax = max_blocks, L_r = ctx_len[r], nb_r = ceil(L_r / B) logical blocks,
+ * n_cand_r = max(nb_r - 1, 0) candidate blocks (the last block, possibly
+ * partial, is the active local block: always attended, never ranked),
+ * local_len_r = L_r - B * n_cand_r tokens in the local block.
+ *
+ * Layouts (row-major, innermost last):
+ *   q            bf16 [R][T][Hq][d]
+ *   host pages   bf16 [NPhys][Hkv][B][d]   Head-Token-Dimension pages (§4.3)
+ *   block table  int32 [R][NBmax]           logical block -> physical page (§4.3)
+ *   kmax, kmin   bf16 [R][Hkv][NBmax][d]
+ *   scores       fp32 [R][Hkv][NBmax]
+ *   sel          int32 [R][Hkv][k]          ascending block ids, -1 padded
+ *   sel_count    int32 [R][Hkv]
+ *   slot_map     int32 [R][Hkv][k]          resident logical block per slot, -1 = free (§4.3)
+ *   slot_stamp   int32 [R][Hkv][k]          decode step at which the slot was last selected (§4.2.3)
+ *   pool_k       bf16 [R][k+1][Hkv][B][d]   HBM working set, keys, token-major per head
+ *   pool_v       bf16 [R][k+1][Hkv][d][B]   HBM working set, values, transposed per head
+ *                (slot k of both pools holds the active local block)
+ *   out          bf16 [R][T][Hq][d]
+ *   lse          fp32 [R][T][Hq]            natural-log log-sum-exp of the scaled logits
+ */
+#ifndef OASIS_H
+#define OASIS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OASIS_ABI_VERSION 1
+
+/* Only the entry points below are exported from liboasis.so. */
+#if defined(__GNUC__) || defined(__clang__)
+#define OASIS_API __attribute__((visibility("default")))
+#else
+#define OASIS_API
+#endif
+
+typedef enum {
+  OASIS_OK = 0,
+  OASIS_ERR_INVALID_ARG = 1,  /* null pointer, inconsistent or out-of-range argument */
+  OASIS_ERR_UNSUPPORTED = 2,  /* valid but not implemented (head_dim != 128, B not 16/32, ...) */
+  OASIS_ERR_HIP = 3,          /* a HIP runtime call or kernel launch failed */
+  OASIS_ERR_WORKSPACE = 4     /* workspace missing or smaller than *_workspace_bytes */
+} oasis_status;
+
+typedef struct {
+  int32_t num_reqs;      /* R   >= 0 (0: every call is a no-op)       */
+  int32_t num_q_heads;   /* Hq  >= 1, multiple of num_kv_heads          */
+  int32_t num_kv_heads;  /* Hkv >= 1                                    */
+  int32_t head_dim;      /* d, must be 128                              */
+  int32_t block_size;    /* B, 16 or 32                                 */
+  int32_t max_blocks;    /* NBmax >= 1: row stride of block table, summaries and scores */
+} oasis_dims;
+
+/* Message for the last non-OK status returned on this thread ("" if none). */
+OASIS_API const char* oasis_last_error(void);
+
+/* OASIS_ABI_VERSION of the loaded library. */
+OASIS_API int32_t oasis_abi_version(void);
+
+/*
+ * Compressed keys (paper §4.2.1 and the "Look-ahead attention" figure: Quest-
+ * style per-block min/max pooling; §5.2: two summary rows per block, 1/16 of
+ * the KV size at B = 16). For every request r, KV head h and candidate block
+ * b < n_cand_r: kmax[r][h][b][:] / kmin[r][h][b][:] = coordinate-wise max /
+ * min of the B keys of logical block b, read from page block_table[r][b].
+ * Rows b >= n_cand_r are not written. The result is exact (bf16 min/max).
+ *
+ * k_pages: device-accessible pages (device memory, or pinned host memory
+ * from hipHostMalloc) [num_pages][Hkv][B][d]. block_table, ctx_len: device.
+ */
+OASIS_API oasis_status oasis_build_summaries(const oasis_dims* dims, const uint16_t* k_pages, int64_t num_pages,
+                                   const int32_t* block_table, const int32_t* ctx_len,
+                                   uint16_t* kmax, uint16_t* kmin, void* stream);
+
+/*
+ * Block importance from the lookahead (draft) queries (paper §4.2.1: each
+ * draft query scans the compressed keys and ranks all logical blocks
+ * independently per KV head). For row q of query head qh, the Quest upper
+ * bound of block b is  sum_d max(q_d * kmin_d, q_d * kmax_d); the score of
+ * (r, h, b) is the maximum of that bound over the rows t in [first_draft,
+ * first_draft + num_draft) and the G query heads of KV head h. Scores of
+ * b in [n_cand_r, NBmax) are -inf. No 1/sqrt(d) factor (ranking only).
+ *
+ * Requires kmin <= kmax coordinate-wise (as built by oasis_build_summaries).
+ * Arithmetic: bf16 products, fp32 accumulation (MFMA). num_draft * G <= 64.
+ * All pointers are device pointers.
+ */
+OASIS_API oasis_status oasis_score_blocks(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens,
+                                int32_t first_draft, int32_t num_draft,
+                                const uint16_t* kmax, const uint16_t* kmin, const int32_t* ctx_len,
+                                float* scores, void* stream);
+
+/*
+ * Top-K selection (paper §4.2.1-§4.2.2: top-K prediction per KV head; §5.2:
+ * K = 128 blocks of 16 tokens = the 2,048-token budget, which is also the
+ * sparsification threshold). For every (r, h): the m = min(k, n_cand_r)
+ * candidates with the largest score, equal scores going to the lower block
+ * id (-0.0 equals +0.0). sel[r][h][0..m) lists them in ascending block id,
+ * sel[r][h][m..k) = -1, sel_count[r][h] = m. Deterministic and exact.
+ * Candidate scores must be finite. 1 <= k <= 65536. Device pointers.
+ */
+OASIS_API oasis_status oasis_select_topk(const oasis_dims* dims, const float* scores, const int32_t* ctx_len,
+                               int32_t k, int32_t* sel, int32_t* sel_count, void* stream);
+
+/* Bytes of workspace oasis_stage_blocks needs for these sizes (0 if invalid). */
+OASIS_API size_t oasis_stage_workspace_bytes(const oasis_dims* dims, int32_t k);
+
+/*
+ * Delta selection + KV transfer into the HBM working set (paper §4.2.3: resident
+ * hits stay and move no bytes; non-selected residents are evicted least-recently-
+ * selected first; each admitted miss is paired with one eviction target; §4.3:
+ * the head-wise slot map records which logical block every slot holds; §5.1: a
+ * gather kernel reads the selected block-head entries from pinned host memory
+ * over PCIe and writes them into the resident GPU pages).
+ *
+ * For every (r, h), with S = sel[r][h][0..sel_count) (ascending, as produced by
+ * oasis_select_topk): misses = S minus the resident blocks (ascending); victims =
+ * free slots (ascending), then resident non-selected slots by (slot_stamp, slot);
+ * the i-th miss goes to the i-th victim: its K entry (B x d) is copied from
+ * host_k page host_block_table[r][block] head h into pool_k[r][slot][h], its V
+ * entry into pool_v[r][slot][h] (transposed to d x B). slot_map is updated and
+ * every slot that holds a selected block afterwards gets slot_stamp = step.
+ * If copy_local != 0, slot k of every head is refreshed from the local block
+ * (logical block nb_r - 1). moved[r][h] (nullable) = entries copied, local
+ * block excluded. A miss whose page id is outside [0, num_pages) is not copied
+ * and its victim slot is left free (-1).
+ *
+ * Local-only form: with sel == NULL and sel_count == NULL (and copy_local = 1)
+ * only slot k is refreshed; slot_map, slot_stamp, moved and the workspace may
+ * then be NULL. This stands in for the model writing the newest token's K/V
+ * into the resident local block before attention.
+ *
+ * fetch_cap: most misses admitted per (r, h) per call; fetch_cap >= k means
+ * uncapped. A cap below k is OASIS_ERR_UNSUPPORTED in this version.
+ * host_k/host_v: pinned host memory (hipHostMalloc) or device memory; the
+ * library resolves the device-visible address. Everything else: device.
+ * sel must be strictly ascending within [0, sel_count); 1 <= k <= 1024.
+ * slot_map must not hold one block twice. Calls that share slot_map/pools
+ * must be ordered on one stream (or by events).
+ */
+OASIS_API oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, const uint16_t* host_v,
+                                int64_t num_pages, const int32_t* host_block_table, const int32_t* ctx_len,
+                                const int32_t* sel, const int32_t* sel_count, int32_t k,
+                                int32_t* slot_map, int32_t* slot_stamp, int32_t step, int32_t fetch_cap,
+                                int32_t copy_local, uint16_t* pool_k, uint16_t* pool_v, int32_t* moved,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of workspace oasis_sparse_decode_attn needs for these sizes (0 if invalid). */
+OASIS_API size_t oasis_attn_workspace_bytes(const oasis_dims* dims, int32_t num_q_tokens, int32_t k_slots);
+
+/*
+ * Block-sparse GQA decode attention over the working set (paper §4.2.1: the
+ * normal and draft queries are stacked and attend one resident KV set in one
+ * call that returns both outputs; §5.2: each head attends its K selected
+ * blocks plus the active local block -- 129 blocks, 2,064 tokens at K = 128,
+ * B = 16). For every request r, query row t and query head qh (KV head
+ * h = qh / G), the attended set is the B tokens of every slot s < k_slots with
+ * slot_map[r][h][s] >= 0, plus the first local_len_r tokens of slot k_slots:
+ *   out = softmax(scale * q . K^T) V,  lse = log sum exp(scale * q . K^T).
+ * No mask among the T rows; an empty set gives out = 0, lse = -inf.
+ * Arithmetic: bf16 inputs, fp32 logits / softmax / accumulation (MFMA), the
+ * probabilities rounded to bf16 for the PV product, bf16 output.
+ * G * T <= 80. lse is nullable. Device pointers.
+ */
+OASIS_API oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens,
+                                      const uint16_t* pool_k, const uint16_t* pool_v,
+                                      const int32_t* slot_map, int32_t k_slots, const int32_t* ctx_len,
+                                      float scale, uint16_t* out, float* lse,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OASIS_H */

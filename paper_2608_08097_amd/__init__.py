@@ -1,0 +1,11 @@
+"""OasisKV decode-time hot path on MI355X (gfx950): HIP kernels behind a C ABI.
+
+The kernels live in ``csrc/`` and build into ``liboasis.so`` (see
+``build_lib.py``); ``_lib`` is the ctypes binding of ``include/oasis.h`` and
+``path`` drives one decode step (score, select, stage, attend) on HIP streams.
+"""
+from ._lib import (  # noqa: F401
+    OasisDims, OasisError, dims, lib, oasis_abi_version, oasis_attn_workspace_bytes,
+    oasis_build_summaries, oasis_last_error, oasis_score_blocks, oasis_select_topk,
+    oasis_sparse_decode_attn, oasis_stage_blocks, oasis_stage_workspace_bytes,
+)

@@ -1,0 +1,236 @@
+"""ctypes binding of liboasis.so: the C ABI declared in include/oasis.h, one
+Python function per entry point, with the same names.
+
+Marshalling only: the functions check that tensors sit where the C ABI expects
+them (device or pinned host), have the right dtype and are contiguous, then
+pass raw pointers and the current HIP stream. Every step of the path runs in
+the library's kernels; there is no fallback. If the library is not built, the
+first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liboasis.so")
+
+STATUS = {0: "OASIS_OK", 1: "OASIS_ERR_INVALID_ARG", 2: "OASIS_ERR_UNSUPPORTED",
+          3: "OASIS_ERR_HIP", 4: "OASIS_ERR_WORKSPACE"}
+
+EXPORTS = (
+    "oasis_last_error", "oasis_abi_version", "oasis_build_summaries", "oasis_score_blocks",
+    "oasis_select_topk", "oasis_stage_workspace_bytes", "oasis_stage_blocks",
+    "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn",
+)
+
+
+class OasisError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn}: {STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class OasisDims(ctypes.Structure):
+    _fields_ = [("num_reqs", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("max_blocks", ctypes.c_int32)]
+
+    def __repr__(self):
+        return "OasisDims(" + ", ".join(f"{n}={getattr(self, n)}" for n, _ in self._fields_) + ")"
+
+
+def dims(num_reqs, num_q_heads, num_kv_heads, head_dim, block_size, max_blocks) -> OasisDims:
+    return OasisDims(int(num_reqs), int(num_q_heads), int(num_kv_heads), int(head_dim), int(block_size),
+                     int(max_blocks))
+
+
+_lib = None
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_SZ = ctypes.c_size_t
+_DIMS = ctypes.POINTER(OasisDims)
+
+
+def lib() -> ctypes.CDLL:
+    """Load liboasis.so (once); raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "or python -m paper_2608_08097_amd.build_lib")
+        L = ctypes.CDLL(LIB_PATH)
+        L.oasis_last_error.restype = ctypes.c_char_p
+        L.oasis_last_error.argtypes = []
+        L.oasis_abi_version.restype = _I32
+        L.oasis_abi_version.argtypes = []
+        L.oasis_build_summaries.restype = _I32
+        L.oasis_build_summaries.argtypes = [_DIMS, _P, _I64, _P, _P, _P, _P, _P]
+        L.oasis_score_blocks.restype = _I32
+        L.oasis_score_blocks.argtypes = [_DIMS, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]
+        L.oasis_select_topk.restype = _I32
+        L.oasis_select_topk.argtypes = [_DIMS, _P, _P, _I32, _P, _P, _P]
+        L.oasis_stage_workspace_bytes.restype = _SZ
+        L.oasis_stage_workspace_bytes.argtypes = [_DIMS, _I32]
+        L.oasis_stage_blocks.restype = _I32
+        L.oasis_stage_blocks.argtypes = [_DIMS, _P, _P, _I64, _P, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
+                                         _P, _P, _P, _P, _SZ, _P]
+        L.oasis_attn_workspace_bytes.restype = _SZ
+        L.oasis_attn_workspace_bytes.argtypes = [_DIMS, _I32, _I32]
+        L.oasis_sparse_decode_attn.restype = _I32
+        L.oasis_sparse_decode_attn.argtypes = [_DIMS, _P, _I32, _P, _P, _P, _I32, _P, ctypes.c_float, _P, _P,
+                                               _P, _SZ, _P]
+        _lib = L
+    return _lib
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise OasisError(fn, status, lib().oasis_last_error().decode())
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _dev(t: torch.Tensor | None, name: str, dtypes, nullable: bool = False):
+    if t is None:
+        if nullable:
+            return None
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype} not in {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _host_or_dev(t: torch.Tensor, name: str, dtypes):
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype} not in {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if not t.is_cuda and not t.is_pinned():
+        raise ValueError(f"{name} must be pinned host memory or a device tensor")
+    return t.data_ptr()
+
+
+def _need(t: torch.Tensor | None, numel: int, name: str) -> None:
+    """Element count the C ABI will address for this argument (no kernel may go past it)."""
+    if t is not None and t.numel() != numel:
+        raise ValueError(f"{name}: {t.numel()} elements, {numel} expected")
+
+
+_BF16 = (torch.bfloat16, torch.uint16, torch.int16)
+_I32T = (torch.int32,)
+_F32 = (torch.float32,)
+
+
+def oasis_abi_version() -> int:
+    return int(lib().oasis_abi_version())
+
+
+def oasis_last_error() -> str:
+    return lib().oasis_last_error().decode()
+
+
+def oasis_build_summaries(d: OasisDims, k_pages, block_table, ctx_len, kmax, kmin, stream=None) -> None:
+    R, H, NB, D = d.num_reqs, d.num_kv_heads, d.max_blocks, d.head_dim
+    _need(k_pages, k_pages.shape[0] * H * d.block_size * D, "k_pages")
+    _need(block_table, R * NB, "block_table")
+    _need(ctx_len, R, "ctx_len")
+    _need(kmax, R * H * NB * D, "kmax")
+    _need(kmin, R * H * NB * D, "kmin")
+    _check("oasis_build_summaries", lib().oasis_build_summaries(
+        ctypes.byref(d), _host_or_dev(k_pages, "k_pages", _BF16), int(k_pages.shape[0]),
+        _dev(block_table, "block_table", _I32T), _dev(ctx_len, "ctx_len", _I32T),
+        _dev(kmax, "kmax", _BF16), _dev(kmin, "kmin", _BF16), _stream(stream)))
+
+
+def oasis_score_blocks(d: OasisDims, q, num_q_tokens: int, first_draft: int, num_draft: int,
+                       kmax, kmin, ctx_len, scores, stream=None) -> None:
+    R, H, NB, D = d.num_reqs, d.num_kv_heads, d.max_blocks, d.head_dim
+    _need(q, R * num_q_tokens * d.num_q_heads * D, "q")
+    _need(kmax, R * H * NB * D, "kmax")
+    _need(kmin, R * H * NB * D, "kmin")
+    _need(ctx_len, R, "ctx_len")
+    _need(scores, R * H * NB, "scores")
+    _check("oasis_score_blocks", lib().oasis_score_blocks(
+        ctypes.byref(d), _dev(q, "q", _BF16), int(num_q_tokens), int(first_draft), int(num_draft),
+        _dev(kmax, "kmax", _BF16), _dev(kmin, "kmin", _BF16), _dev(ctx_len, "ctx_len", _I32T),
+        _dev(scores, "scores", _F32), _stream(stream)))
+
+
+def oasis_select_topk(d: OasisDims, scores, ctx_len, k: int, sel, sel_count, stream=None) -> None:
+    R, H = d.num_reqs, d.num_kv_heads
+    _need(scores, R * H * d.max_blocks, "scores")
+    _need(ctx_len, R, "ctx_len")
+    _need(sel, R * H * k, "sel")
+    _need(sel_count, R * H, "sel_count")
+    _check("oasis_select_topk", lib().oasis_select_topk(
+        ctypes.byref(d), _dev(scores, "scores", _F32), _dev(ctx_len, "ctx_len", _I32T), int(k),
+        _dev(sel, "sel", _I32T), _dev(sel_count, "sel_count", _I32T), _stream(stream)))
+
+
+def oasis_stage_workspace_bytes(d: OasisDims, k: int) -> int:
+    return int(lib().oasis_stage_workspace_bytes(ctypes.byref(d), int(k)))
+
+
+def oasis_stage_blocks(d: OasisDims, host_k, host_v, host_block_table, ctx_len, sel, sel_count, k: int,
+                       slot_map, slot_stamp, step: int, fetch_cap: int, copy_local: bool, pool_k, pool_v,
+                       moved, workspace, stream=None) -> None:
+    if host_k.shape != host_v.shape:
+        raise ValueError("host_k and host_v differ in shape")
+    R, H, B, D = d.num_reqs, d.num_kv_heads, d.block_size, d.head_dim
+    _need(host_k, host_k.shape[0] * H * B * D, "host_k")
+    _need(host_block_table, R * d.max_blocks, "host_block_table")
+    _need(ctx_len, R, "ctx_len")
+    for t, n in ((sel, "sel"), (slot_map, "slot_map"), (slot_stamp, "slot_stamp")):
+        _need(t, R * H * k, n)
+    _need(sel_count, R * H, "sel_count")
+    _need(moved, R * H, "moved")
+    _need(pool_k, R * (k + 1) * H * B * D, "pool_k")
+    _need(pool_v, R * (k + 1) * H * B * D, "pool_v")
+    _check("oasis_stage_blocks", lib().oasis_stage_blocks(
+        ctypes.byref(d), _host_or_dev(host_k, "host_k", _BF16), _host_or_dev(host_v, "host_v", _BF16),
+        int(host_k.shape[0]), _dev(host_block_table, "host_block_table", _I32T), _dev(ctx_len, "ctx_len", _I32T),
+        _dev(sel, "sel", _I32T, nullable=True), _dev(sel_count, "sel_count", _I32T, nullable=True), int(k),
+        _dev(slot_map, "slot_map", _I32T, nullable=True), _dev(slot_stamp, "slot_stamp", _I32T, nullable=True),
+        int(step), int(fetch_cap), 1 if copy_local else 0, _dev(pool_k, "pool_k", _BF16),
+        _dev(pool_v, "pool_v", _BF16), _dev(moved, "moved", _I32T, nullable=True),
+        _dev(workspace, "workspace", (torch.uint8,), nullable=True),
+        0 if workspace is None else int(workspace.numel()), _stream(stream)))
+
+
+def oasis_attn_workspace_bytes(d: OasisDims, num_q_tokens: int, k_slots: int) -> int:
+    return int(lib().oasis_attn_workspace_bytes(ctypes.byref(d), int(num_q_tokens), int(k_slots)))
+
+
+def oasis_sparse_decode_attn(d: OasisDims, q, num_q_tokens: int, pool_k, pool_v, slot_map, k_slots: int,
+                             ctx_len, scale: float | None, out, lse, workspace, stream=None) -> None:
+    if scale is None:
+        scale = 1.0 / math.sqrt(d.head_dim)
+    R, H, B, D = d.num_reqs, d.num_kv_heads, d.block_size, d.head_dim
+    _need(q, R * num_q_tokens * d.num_q_heads * D, "q")
+    _need(out, R * num_q_tokens * d.num_q_heads * D, "out")
+    _need(lse, R * num_q_tokens * d.num_q_heads, "lse")
+    _need(pool_k, R * (k_slots + 1) * H * B * D, "pool_k")
+    _need(pool_v, R * (k_slots + 1) * H * B * D, "pool_v")
+    _need(slot_map, R * H * k_slots, "slot_map")
+    _need(ctx_len, R, "ctx_len")
+    _check("oasis_sparse_decode_attn", lib().oasis_sparse_decode_attn(
+        ctypes.byref(d), _dev(q, "q", _BF16), int(num_q_tokens), _dev(pool_k, "pool_k", _BF16),
+        _dev(pool_v, "pool_v", _BF16), _dev(slot_map, "slot_map", _I32T, nullable=k_slots == 0), int(k_slots),
+        _dev(ctx_len, "ctx_len", _I32T), float(scale), _dev(out, "out", _BF16),
+        _dev(lse, "lse", _F32, nullable=True), _dev(workspace, "workspace", (torch.uint8,)),
+        int(workspace.numel()), _stream(stream)))

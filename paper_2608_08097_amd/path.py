@@ -1,0 +1,140 @@
+"""One layer of the OasisKV decode path: device buffers and the stream schedule.
+
+Paper §4.2.2: at every decode step the foreground runs attention of the stacked
+queries over the current working set while a background stream turns the draft
+queries into the next working set (top-K prediction -> KV selection -> KV
+transfer); events keep the dependencies of each layer. This module owns the
+buffers of one layer and issues the library calls in that order; every
+computation happens in liboasis.so (through ``_lib``). PyTorch provides device
+memory, pinned host memory, streams and events.
+"""
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import _lib as L
+
+
+class LayerState:
+    """HBM state of one layer: compressed keys, scores, selection, slot map, pools."""
+
+    def __init__(self, d: L.OasisDims, num_q_tokens: int, k: int, device: str | torch.device = "cuda"):
+        R, Hq, Hkv, D, B, NB = (d.num_reqs, d.num_q_heads, d.num_kv_heads, d.head_dim, d.block_size,
+                               d.max_blocks)
+        self.dims, self.T, self.k = d, int(num_q_tokens), int(k)
+        dev = torch.device(device)
+        bf = torch.bfloat16
+        i32 = torch.int32
+        self.kmax = torch.empty((R, Hkv, NB, D), dtype=bf, device=dev)
+        self.kmin = torch.empty((R, Hkv, NB, D), dtype=bf, device=dev)
+        self.scores = torch.empty((R, Hkv, NB), dtype=torch.float32, device=dev)
+        self.sel = torch.empty((R, Hkv, k), dtype=i32, device=dev)
+        self.sel_count = torch.empty((R, Hkv), dtype=i32, device=dev)
+        self.slot_map = torch.full((R, Hkv, k), -1, dtype=i32, device=dev)
+        self.slot_stamp = torch.zeros((R, Hkv, k), dtype=i32, device=dev)
+        self.pool_k = torch.zeros((R, k + 1, Hkv, B, D), dtype=bf, device=dev)
+        self.pool_v = torch.zeros((R, k + 1, Hkv, D, B), dtype=bf, device=dev)
+        self.moved = torch.zeros((R, Hkv), dtype=i32, device=dev)
+        self.out = torch.empty((R, self.T, Hq, D), dtype=bf, device=dev)
+        self.lse = torch.empty((R, self.T, Hq), dtype=torch.float32, device=dev)
+        self.ws_stage = torch.empty(max(1, L.oasis_stage_workspace_bytes(d, k)), dtype=torch.uint8, device=dev)
+        self.ws_attn = torch.empty(max(1, L.oasis_attn_workspace_bytes(d, self.T, k)), dtype=torch.uint8,
+                                   device=dev)
+        self.ev_staged = None   # recorded after the last stage of this layer
+        self.ev_attended = None  # recorded after the last attention of this layer
+
+    def reset(self):
+        self.slot_map.fill_(-1)
+        self.slot_stamp.zero_()
+
+
+class DecodePath:
+    """Issues score -> select -> stage -> attend for one layer on HIP streams.
+
+    ``host_k``/``host_v`` are the pinned host tier (bf16 pages
+    ``[NPhys][Hkv][B][d]``), ``block_table`` the device page table
+    ``[R][NBmax]``.
+    """
+
+    def __init__(self, d: L.OasisDims, num_q_tokens: int, k: int, host_k: torch.Tensor, host_v: torch.Tensor,
+                 block_table: torch.Tensor, first_draft: int = 1, num_draft: int | None = None,
+                 scale: float | None = None):
+        self.dims, self.T, self.k = d, int(num_q_tokens), int(k)
+        self.first_draft = int(first_draft)
+        self.num_draft = int(num_draft if num_draft is not None else self.T - self.first_draft)
+        self.host_k, self.host_v, self.block_table = host_k, host_v, block_table
+        self.scale = scale if scale is not None else 1.0 / math.sqrt(d.head_dim)
+        self.side = torch.cuda.Stream()  # default priority
+
+    def new_layer(self) -> LayerState:
+        return LayerState(self.dims, self.T, self.k, self.block_table.device)
+
+    # -- individual steps (all asynchronous on `stream`) ----------------------
+    def build_summaries(self, st: LayerState, ctx_len: torch.Tensor, k_pages: torch.Tensor | None = None,
+                        stream=None):
+        L.oasis_build_summaries(self.dims, self.host_k if k_pages is None else k_pages, self.block_table,
+                                ctx_len, st.kmax, st.kmin, stream)
+
+    def predict(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, stream=None):
+        L.oasis_score_blocks(self.dims, q, self.T, self.first_draft, self.num_draft, st.kmax, st.kmin, ctx_len,
+                             st.scores, stream)
+        L.oasis_select_topk(self.dims, st.scores, ctx_len, self.k, st.sel, st.sel_count, stream)
+
+    def stage(self, st: LayerState, ctx_len: torch.Tensor, step: int, stream=None, fetch_cap: int | None = None,
+              copy_local: bool = True):
+        L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, st.sel, st.sel_count,
+                             self.k, st.slot_map, st.slot_stamp, step, self.k if fetch_cap is None else fetch_cap,
+                             copy_local, st.pool_k, st.pool_v, st.moved, st.ws_stage, stream)
+
+    def refresh_local(self, st: LayerState, ctx_len: torch.Tensor, stream=None):
+        """Write the active local block into slot k (stands in for the model's KV write)."""
+        L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, None, None, self.k,
+                             None, None, 0, self.k, True, st.pool_k, st.pool_v, None, None, stream)
+
+    def attend(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, stream=None):
+        L.oasis_sparse_decode_attn(self.dims, q, self.T, st.pool_k, st.pool_v, st.slot_map, self.k, ctx_len,
+                                   self.scale, st.out, st.lse, st.ws_attn, stream)
+
+    # -- schedules --------------------------------------------------------------
+    def step_serial(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, step: int):
+        """predict -> stage -> attend on the current stream: attention uses this step's selection."""
+        self.predict(st, q, ctx_len)
+        self.stage(st, ctx_len, step)
+        self.attend(st, q, ctx_len)
+
+    def step_pipelined(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, step: int,
+                       growing: bool = False):
+        """One steady-state step (paper §4.2.2, one layer).
+
+        Foreground (current stream): wait for this layer's previous transfer,
+        then attention of all T rows over the working set it produced.
+        Background (side stream): score + select from the draft rows of ``q``
+        concurrently with the attention, then, once the attention no longer
+        reads the pools, stage the new selection for the next step.
+        With ``growing`` (one token appended per step) the local block is
+        rewritten on the foreground before the attention, since it changes
+        every step; otherwise the background stage refreshes it.
+        """
+        fg = torch.cuda.current_stream()
+        bg = self.side
+        ev_q = torch.cuda.Event()
+        ev_q.record(fg)  # q and ctx_len are ready on the foreground
+        bg.wait_event(ev_q)
+        if st.ev_staged is not None:
+            fg.wait_event(st.ev_staged)
+        if growing:
+            self.refresh_local(st, ctx_len, fg)
+        self.attend(st, q, ctx_len, fg)
+        ev_attn = torch.cuda.Event()
+        ev_attn.record(fg)
+        self.predict(st, q, ctx_len, bg)
+        bg.wait_event(ev_attn)  # the gather overwrites slots the attention reads
+        self.stage(st, ctx_len, step, bg, copy_local=not growing)
+        ev_staged = torch.cuda.Event()
+        ev_staged.record(bg)
+        st.ev_staged, st.ev_attended = ev_staged, ev_attn
+
+    def join(self):
+        torch.cuda.current_stream().wait_stream(self.side)

@@ -1,0 +1,89 @@
+"""The C-ABI library loads and exports every symbol include/oasis.h declares (CPU only).
+
+No compute call is made here; argument checks that fail before any HIP call
+are exercised through ctypes.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "oasis.h")
+LIB = os.path.join(ROOT, "paper_2608_08097_amd", "liboasis.so")
+
+
+def declared():
+    txt = open(HEADER).read()
+    return sorted(set(re.findall(r"^OASIS_API\s+[\w\s\*]+?\b(oasis_\w+)\s*\(", txt, re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB):
+        from paper_2608_08097_amd.build_lib import build
+        build()
+    import paper_2608_08097_amd as P
+    return P
+
+
+def test_header_declares_the_path():
+    names = declared()
+    for fn in ("oasis_score_blocks", "oasis_select_topk", "oasis_stage_blocks", "oasis_sparse_decode_attn",
+               "oasis_build_summaries", "oasis_attn_workspace_bytes", "oasis_stage_workspace_bytes",
+               "oasis_last_error", "oasis_abi_version"):
+        assert fn in names
+
+
+def test_exports_match_header(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True, check=True).stdout
+    exported = sorted({l.split()[-1] for l in out.splitlines() if l.split() and l.split()[-1].startswith("oasis_")})
+    assert exported == declared()
+    cdll = ctypes.CDLL(LIB)
+    for fn in declared():
+        assert hasattr(cdll, fn)
+    assert sorted(lib._lib.EXPORTS) == declared()
+
+
+def test_abi_version(lib):
+    assert lib.oasis_abi_version() == 1
+
+
+def test_argument_checks_without_gpu(lib):
+    L = lib.lib()
+    bad_hd = lib.dims(1, 32, 8, 64, 16, 512)
+    assert L.oasis_score_blocks(ctypes.byref(bad_hd), None, 5, 1, 4, None, None, None, None, None) == 2
+    assert "head_dim" in lib.oasis_last_error()
+    bad_b = lib.dims(1, 32, 8, 128, 8, 512)
+    assert L.oasis_select_topk(ctypes.byref(bad_b), None, None, 4, None, None, None) == 2
+    bad_g = lib.dims(1, 30, 8, 128, 16, 512)
+    assert L.oasis_sparse_decode_attn(ctypes.byref(bad_g), None, 5, None, None, None, 4, None, 1.0, None, None,
+                                      None, 0, None) == 1
+    d = lib.dims(1, 32, 8, 128, 16, 512)
+    assert L.oasis_score_blocks(ctypes.byref(d), None, 5, 1, 4, None, None, None, None, None) == 1
+    assert "q is NULL" in lib.oasis_last_error()
+    assert L.oasis_score_blocks(ctypes.byref(d), None, 5, 2, 4, None, None, None, None, None) == 1  # rows past T
+    assert L.oasis_select_topk(ctypes.byref(d), None, None, 0, None, None, None) == 1
+    rows65 = lib.dims(1, 72, 8, 128, 16, 512)  # G = 9, D = 8 -> 72 scoring rows
+    assert L.oasis_score_blocks(ctypes.byref(rows65), None, 9, 1, 8, None, None, None, None, None) == 2
+    big = lib.dims(1, 96, 8, 128, 16, 512)     # G = 12, T = 9 -> 108 attention rows
+    assert L.oasis_sparse_decode_attn(ctypes.byref(big), None, 9, None, None, None, 4, None, 1.0, None, None,
+                                      None, 0, None) == 2
+    # capped eviction is not implemented yet: explicit UNSUPPORTED
+    assert L.oasis_stage_blocks(ctypes.byref(d), None, None, 10, None, None, None, None, 128, None, None, 0, 6, 1,
+                                None, None, None, None, 0, None) == 2
+    # zero requests: a no-op that succeeds without touching the device
+    z = lib.dims(0, 32, 8, 128, 16, 512)
+    assert L.oasis_score_blocks(ctypes.byref(z), None, 5, 1, 4, None, None, None, None, None) == 0
+    assert lib.oasis_last_error() == ""
+
+
+def test_workspace_sizes(lib):
+    d = lib.dims(8, 32, 8, 128, 16, 8192)
+    ws = lib.oasis_attn_workspace_bytes(d, 5, 128)
+    assert ws > 0 and ws % 4 == 0
+    assert lib.oasis_stage_workspace_bytes(d, 128) == 8 * 8 * 128 * 8 + 8 * 8 * 4
+    assert lib.oasis_stage_workspace_bytes(d, 2048) == 0       # k above the plan kernel's limit
+    assert lib.oasis_attn_workspace_bytes(lib.dims(1, 32, 8, 64, 16, 1), 5, 4) == 0

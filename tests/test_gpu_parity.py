@@ -1,0 +1,374 @@
+"""GPU parity: every kernel of the decode path through the C ABI vs the CPU oracle.
+
+Sizes are chosen so the oracle finishes in seconds while the kernels still see
+several tiles, splits and a ragged tail (contexts that are not multiples of
+the block size or of the 16-block scoring tile, budgets larger than the
+candidate count, empty and one-token contexts).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_08097_amd as P
+from oracle import oasis_oracle as O
+from paper_2608_08097_amd.path import DecodePath, LayerState
+from tests.gpu_util import (as_np_bits, assert_attn_close, assert_lse_close, assert_scores_close, dev_bf16,
+                            dev_i32, host_bits, note, oracle_layer, pinned_pages, pool_v_from_htd, pool_v_to_htd,
+                            selection_diff)
+from workloads import (config, f32_to_bf16_bits, make_workload, random_bf16, random_scores,
+                       random_selection, random_selection_h)
+
+pytestmark = pytest.mark.gpu
+
+
+def _dims(w):
+    c = w.cfg
+    return P.dims(c.num_reqs, c.num_q_heads, c.num_kv_heads, c.head_dim, c.block_size, w.NBmax)
+
+
+def _summ_bits(x):
+    """Oracle summaries (exact bf16 values, NaN where undefined) -> bf16 bits."""
+    return f32_to_bf16_bits(np.nan_to_num(x, nan=0.0).astype(np.float32))
+
+
+CASES = {
+    # ragged contexts from 1 token to a few hundred blocks, B = 16
+    "ragged16": lambda: make_workload("c2", num_reqs=5, ctx_args=(1, 3000), budget=512),
+    "c1": lambda: make_workload("c1"),
+    # B = 32, 64 scoring rows (G = 8, D = 8), 72 attention rows
+    "gqa8_b32": lambda: make_workload("c5", num_reqs=2, ctx_args=(3000,), budget=1024),
+    # G = 4, D = 1: 4 scoring rows (padded tile), 8 attention rows
+    "d1": lambda: make_workload("c1", num_draft=1, ctx_args=(2500,), budget=256),
+    # one KV head group with 2 query heads, D = 2
+    "g2": lambda: make_workload("c2", num_reqs=3, num_q_heads=16, num_draft=2, ctx_args=(700, 2200), budget=320),
+}
+
+
+@pytest.fixture(scope="module", params=sorted(CASES))
+def case(request):
+    note(f"building inputs for {request.param}")
+    w = CASES[request.param]()
+    hk_t, hv_t = pinned_pages(w)
+    return request.param, w, hk_t, hv_t
+
+
+# ---------------------------------------------------------------------------
+# a0 summaries: bit-exact
+# ---------------------------------------------------------------------------
+
+def test_summaries_bit_exact(case):
+    name, w, hk_t, hv_t = case
+    c = w.cfg
+    d = _dims(w)
+    ctx = w.ctx_len(0)
+    ref_max, ref_min = O.block_summaries(as_np_bits(hk_t), w.block_table, ctx, c.block_size, w.NBmax)
+    for source in ("pinned", "device"):
+        note(f"summaries {name} from {source} pages")
+        pages = hk_t if source == "pinned" else hk_t.cuda()
+        kmax = torch.zeros((c.num_reqs, c.num_kv_heads, w.NBmax, c.head_dim), dtype=torch.bfloat16, device="cuda")
+        kmin = torch.zeros_like(kmax)
+        P.oasis_build_summaries(d, pages, dev_i32(w.block_table), dev_i32(ctx), kmax, kmin)
+        torch.cuda.synchronize()
+        gmax, gmin = O.bf16_to_f64(host_bits(kmax)), O.bf16_to_f64(host_bits(kmin))
+        for r in range(c.num_reqs):
+            _, nc, _ = O.block_counts(ctx[r], c.block_size)
+            assert np.array_equal(gmax[r, :, :nc], ref_max[r, :, :nc]), (r, "kmax")
+            assert np.array_equal(gmin[r, :, :nc], ref_min[r, :, :nc]), (r, "kmin")
+            assert np.all(gmax[r, :, nc:] == 0), "rows past the candidates must stay untouched"
+
+
+# ---------------------------------------------------------------------------
+# a1 scores on the oracle's summaries
+# ---------------------------------------------------------------------------
+
+def test_scores(case):
+    name, w, hk_t, _ = case
+    c = w.cfg
+    d = _dims(w)
+    ctx = w.ctx_len(0)
+    q = w.queries(0)
+    kmax, kmin = O.block_summaries(as_np_bits(hk_t), w.block_table, ctx, c.block_size, w.NBmax)
+    ref = O.block_scores(q, kmax, kmin, ctx, c.num_kv_heads, c.block_size)
+    note(f"scores {name}")
+    scores = torch.full((c.num_reqs, c.num_kv_heads, w.NBmax), 7.0, device="cuda")
+    P.oasis_score_blocks(d, dev_bf16(q), c.T, 1, c.num_draft, dev_bf16(_summ_bits(kmax)), dev_bf16(_summ_bits(kmin)),
+                         dev_i32(ctx), scores)
+    torch.cuda.synchronize()
+    assert_scores_close(scores.cpu().numpy(), ref)
+
+
+# ---------------------------------------------------------------------------
+# a2 selection on given scores: bit-exact
+# ---------------------------------------------------------------------------
+
+SELECT_CASES = [
+    # (seed, R, H, NBmax, B, ctx lengths, k, n_distinct)
+    (1, 3, 8, 700, 16, [16 * 700, 16 * 300 + 5, 16 * 129], 128, None),
+    (2, 2, 8, 9000, 16, [16 * 9000, 16 * 8192], 128, None),
+    (3, 4, 2, 600, 16, [9600, 16, 1, 0], 64, None),           # one candidate, none, empty
+    (4, 3, 4, 520, 16, [8320, 8000, 4000], 128, 5),           # heavy ties: 5 distinct values
+    (5, 2, 8, 300, 32, [9600, 9000], 1, 3),                   # k = 1 with ties
+    (6, 2, 3, 2100, 32, [67200, 50000], 256, None),
+    (7, 1, 1, 64, 16, [1024], 4096, None),                    # k far above the candidates
+    (8, 2, 2, 5000, 16, [80000, 80000], 4000, 50),            # large k, ties
+]
+
+
+@pytest.mark.parametrize("seed,R,H,NB,B,lens,k,nd", SELECT_CASES)
+def test_select_exact(seed, R, H, NB, B, lens, k, nd):
+    scores = random_scores(300 + seed, (R, H, NB), n_distinct=nd)
+    if seed % 2:  # signed zeros must compare equal
+        scores[..., ::7] = np.float32(-0.0)
+        scores[..., 3::7] = np.float32(0.0)
+    ctx = np.array(lens, np.int32)
+    ref_sel, ref_cnt = O.select_topk(scores, ctx, k, B)
+    note(f"select seed={seed} R={R} H={H} NB={NB} k={k}")
+    d = P.dims(R, 8 * H, H, 128, B, NB)
+    sel = torch.full((R, H, k), -7, dtype=torch.int32, device="cuda")
+    cnt = torch.full((R, H), -7, dtype=torch.int32, device="cuda")
+    P.oasis_select_topk(d, torch.from_numpy(scores).cuda(), dev_i32(ctx), k, sel, cnt)
+    torch.cuda.synchronize()
+    assert np.array_equal(cnt.cpu().numpy(), ref_cnt)
+    assert np.array_equal(sel.cpu().numpy(), ref_sel)
+
+
+# ---------------------------------------------------------------------------
+# a3 staging: plan (slot map, stamps, counts) and bytes, bit-exact
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("copy_local", [True, False])
+def test_stage_exact(case, copy_local):
+    name, w, hk_t, hv_t = case
+    c = w.cfg
+    d = _dims(w)
+    ctx = w.ctx_len(0)
+    k = c.K
+    n_cand = np.array([O.block_counts(L, c.block_size)[1] for L in ctx])
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table))
+    st = LayerState(d, c.T, k)
+    hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
+    smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
+    stamp = np.zeros_like(smap)
+    pk = np.zeros((c.num_reqs, k + 1, c.num_kv_heads, c.block_size, c.head_dim), np.uint16)
+    pv = np.zeros_like(pk)
+    sel, cnt = random_selection_h(500, n_cand, c.num_kv_heads, k)
+    ctx_d = dev_i32(ctx)
+    for step in range(1, 5):
+        if step == 3:
+            pass  # same selection again: nothing may move
+        elif step > 1:
+            sel, cnt = random_selection(500 + step, n_cand, k, prev=(sel, cnt), keep_frac=0.6)
+        moved = O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, step, pk, pv, ctx, c.block_size,
+                               copy_local=copy_local)
+        note(f"stage {name} step={step} copy_local={copy_local}")
+        st.sel.copy_(torch.from_numpy(sel))
+        st.sel_count.copy_(torch.from_numpy(cnt))
+        path.stage(st, ctx_d, step, copy_local=copy_local)
+        torch.cuda.synchronize()
+        assert np.array_equal(st.slot_map.cpu().numpy(), smap), step
+        assert np.array_equal(st.slot_stamp.cpu().numpy(), stamp), step
+        assert np.array_equal(st.moved.cpu().numpy(), moved), step
+        if step == 3:
+            assert moved.sum() == 0
+        assert np.array_equal(host_bits(st.pool_k), pk), step
+        assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv), step
+
+
+def test_stage_local_only(case):
+    name, w, hk_t, hv_t = case
+    c = w.cfg
+    d = _dims(w)
+    ctx = w.ctx_len(0)
+    k = c.K
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table))
+    st = LayerState(d, c.T, k)
+    note(f"stage local-only {name}")
+    path.refresh_local(st, dev_i32(ctx))
+    torch.cuda.synchronize()
+    pk = np.zeros((c.num_reqs, k + 1, c.num_kv_heads, c.block_size, c.head_dim), np.uint16)
+    pv = np.zeros_like(pk)
+    smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
+    O.stage_blocks(as_np_bits(hk_t), as_np_bits(hv_t), w.block_table, np.full_like(smap, -1),
+                   np.zeros((c.num_reqs, c.num_kv_heads), np.int32), smap, np.zeros_like(smap), 0, pk, pv, ctx,
+                   c.block_size, copy_local=True)
+    assert np.array_equal(host_bits(st.pool_k), pk)
+    assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv)
+    assert np.all(st.slot_map.cpu().numpy() == -1)
+
+
+# ---------------------------------------------------------------------------
+# a4 attention on random pools and slot maps
+# ---------------------------------------------------------------------------
+
+ATTN_CASES = [
+    # (seed, R, Hq, Hkv, T, B, k_slots, ctx lengths, free fraction)
+    (1, 2, 32, 8, 5, 16, 128, [131072, 2000], 0.0),
+    (2, 3, 32, 8, 5, 16, 7, [100, 17, 16], 0.3),         # odd unit tail, local_len 1 and 16
+    (3, 2, 64, 8, 9, 32, 128, [65536, 33], 0.2),         # 72 rows, B = 32
+    (4, 2, 8, 8, 1, 16, 40, [5000, 5001], 0.5),          # 1 row per head (T = 1, G = 1)
+    (5, 2, 32, 8, 5, 16, 0, [10, 1], 0.0),               # local block only
+    (6, 2, 32, 8, 5, 16, 16, [0, 300], 1.0),             # empty context; all slots free
+    (7, 1, 40, 8, 4, 16, 300, [8192], 0.1),              # G = 5: 20 rows, many splits
+    (8, 2, 16, 2, 5, 32, 33, [1000, 64], 0.25),
+]
+
+
+@pytest.mark.parametrize("seed,R,Hq,Hkv,T,B,ks,lens,free", ATTN_CASES)
+def test_attn(seed, R, Hq, Hkv, T, B, ks, lens, free):
+    d_head = 128
+    q = random_bf16(700 + seed, (R, T, Hq, d_head))
+    pk = random_bf16(710 + seed, (R, ks + 1, Hkv, B, d_head))
+    pv = random_bf16(720 + seed, (R, ks + 1, Hkv, B, d_head))
+    rng = np.random.default_rng(730 + seed)
+    smap = np.where(rng.random((R, Hkv, ks)) < free, -1, rng.integers(0, 10 ** 6, (R, Hkv, ks))).astype(np.int32)
+    ctx = np.array(lens, np.int32)
+    # garbage (NaN bf16) in free slots and past the local block's end must not leak
+    nan = np.uint16(0x7FC0)
+    for r in range(R):
+        for h in range(Hkv):
+            for s in range(ks):
+                if smap[r, h, s] < 0:
+                    pk[r, s, h] = nan
+                    pv[r, s, h] = nan
+        _, _, ll = O.block_counts(ctx[r], B)
+        pk[r, ks, :, ll:] = nan
+        pv[r, ks, :, ll:] = nan
+    ref_o, ref_l = O.sparse_attend(q, pk, pv, smap, ctx, B)
+    note(f"attn seed={seed} R={R} Hq={Hq} Hkv={Hkv} T={T} B={B} ks={ks}")
+    d = P.dims(R, Hq, Hkv, d_head, B, max(1, (int(ctx.max()) + B - 1) // B))
+    out = torch.zeros((R, T, Hq, d_head), dtype=torch.bfloat16, device="cuda")
+    lse = torch.zeros((R, T, Hq), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.oasis_attn_workspace_bytes(d, T, ks), dtype=torch.uint8, device="cuda")
+    P.oasis_sparse_decode_attn(d, dev_bf16(q), T, dev_bf16(pk), dev_bf16(pool_v_from_htd(pv)),
+                               dev_i32(smap) if ks else None, ks, dev_i32(ctx), None, out, lse, ws)
+    torch.cuda.synchronize()
+    assert_attn_close(host_bits(out), ref_o)
+    assert_lse_close(lse.cpu().numpy(), ref_l)
+
+
+# ---------------------------------------------------------------------------
+# the whole step (summaries -> scores -> selection -> staging -> attention)
+# ---------------------------------------------------------------------------
+
+def test_full_step(case):
+    name, w, hk_t, hv_t = case
+    c = w.cfg
+    d = _dims(w)
+    ctx = w.ctx_len(0)
+    q = w.queries(0)
+    k = c.K
+    ref = oracle_layer(w, as_np_bits(hk_t), as_np_bits(hv_t), ctx, q, k)
+    note(f"full step {name}")
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table))
+    st = LayerState(d, c.T, k)
+    ctx_d, q_d = dev_i32(ctx), dev_bf16(q)
+    path.build_summaries(st, ctx_d)
+    path.step_serial(st, q_d, ctx_d, 0)
+    torch.cuda.synchronize()
+    assert_scores_close(st.scores.cpu().numpy(), ref["scores"])
+    swapped = selection_diff(st.sel.cpu().numpy(), st.sel_count.cpu().numpy(), ref["sel"], ref["cnt"],
+                             ref["scores"])
+    assert not swapped, f"near-tie swaps in {swapped}"
+    if c.key_dist == "planted":
+        sel = st.sel.cpu().numpy()
+        for r in range(c.num_reqs):
+            for h in range(c.num_kv_heads):
+                assert set(w.planted_ids(r, h)) <= set(sel[r, h]), (r, h)
+    assert np.array_equal(st.slot_map.cpu().numpy(), ref["slot_map"])
+    assert np.array_equal(st.moved.cpu().numpy(), ref["moved"])
+    assert_attn_close(host_bits(st.out), ref["out"])
+    assert_lse_close(st.lse.cpu().numpy(), ref["lse"])
+
+
+def test_dense_equivalence():
+    """Budget above every context: the sparse path reproduces dense attention (paper §5.2 threshold)."""
+    w = make_workload("c2", num_reqs=3, ctx_args=(100, 1500), budget=16 * 100)
+    c = w.cfg
+    hk_t, hv_t = pinned_pages(w)
+    d = _dims(w)
+    ctx = w.ctx_len(0)
+    k = w.NBmax
+    note("dense equivalence")
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table))
+    st = LayerState(d, c.T, k)
+    ctx_d, q_d = dev_i32(ctx), dev_bf16(w.queries(0))
+    path.build_summaries(st, ctx_d)
+    path.step_serial(st, q_d, ctx_d, 0)
+    torch.cuda.synchronize()
+    ref_o, ref_l = O.dense_attend(w.queries(0), as_np_bits(hk_t), as_np_bits(hv_t), w.block_table, ctx, c.block_size)
+    assert_attn_close(host_bits(st.out), ref_o)
+    assert_lse_close(st.lse.cpu().numpy(), ref_l)
+
+
+def test_pipelined_multistep():
+    """Reasoning-style loop: AR(1) queries, one token per step, attention on the previous step's staging."""
+    steps = 6
+    w = make_workload("c3", num_reqs=3, ctx_args=(200, 300, 1400), steps=steps, budget=16 * 24)
+    c = w.cfg
+    hk_t, hv_t = pinned_pages(w)
+    hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
+    d = _dims(w)
+    k = c.K
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table))
+    st = LayerState(d, c.T, k)
+    smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
+    stamp = np.zeros_like(smap)
+    pk = np.zeros((c.num_reqs, k + 1, c.num_kv_heads, c.block_size, c.head_dim), np.uint16)
+    pv = np.zeros_like(pk)
+    none_sel = np.full_like(smap, -1)
+    zero_cnt = np.zeros((c.num_reqs, c.num_kv_heads), np.int32)
+    for s in range(steps):
+        ctx = w.ctx_len(s)
+        q = w.queries(s)
+        # oracle, same schedule: local block, attention, then prediction and staging for the next step
+        O.stage_blocks(hk, hv, w.block_table, none_sel, zero_cnt, smap, stamp, s, pk, pv, ctx, c.block_size)
+        ref_o, ref_l = O.sparse_attend(q, pk, pv, smap, ctx, c.block_size)
+        kmax, kmin = O.block_summaries(hk, w.block_table, ctx, c.block_size, w.NBmax)
+        sc = O.block_scores(q, kmax, kmin, ctx, c.num_kv_heads, c.block_size)
+        sel, cnt = O.select_topk(sc, ctx, k, c.block_size)
+        moved = O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, s, pk, pv, ctx, c.block_size,
+                               copy_local=False)
+        note(f"pipelined step {s}")
+        ctx_d, q_d = dev_i32(ctx), dev_bf16(q)
+        path.build_summaries(st, ctx_d)   # summaries of blocks completed so far
+        path.step_pipelined(st, q_d, ctx_d, s, growing=True)
+        path.join()
+        torch.cuda.synchronize()
+        assert_attn_close(host_bits(st.out), ref_o, f"step {s} out")
+        assert_lse_close(st.lse.cpu().numpy(), ref_l)
+        assert not selection_diff(st.sel.cpu().numpy(), st.sel_count.cpu().numpy(), sel, cnt, sc)
+        assert np.array_equal(st.slot_map.cpu().numpy(), smap), s
+        assert np.array_equal(st.slot_stamp.cpu().numpy(), stamp), s
+        assert np.array_equal(st.moved.cpu().numpy(), moved), s
+        if s > 0:
+            assert moved.sum() < cnt.sum(), "AR(1) drift: later steps are deltas"
+
+
+# ---------------------------------------------------------------------------
+# host-side errors through the C ABI on a GPU machine
+# ---------------------------------------------------------------------------
+
+def test_abi_errors_on_device():
+    d = P.dims(1, 32, 8, 128, 16, 16)
+    T, k = 5, 4
+    q = torch.zeros((1, T, 32, 128), dtype=torch.bfloat16, device="cuda")
+    pool = torch.zeros((1, k + 1, 8, 16, 128), dtype=torch.bfloat16, device="cuda")
+    smap = torch.full((1, 8, k), -1, dtype=torch.int32, device="cuda")
+    ctx = torch.ones(1, dtype=torch.int32, device="cuda")
+    out = torch.zeros((1, T, 32, 128), dtype=torch.bfloat16, device="cuda")
+    small = torch.empty(8, dtype=torch.uint8, device="cuda")
+    with pytest.raises(P.OasisError) as e:
+        P.oasis_sparse_decode_attn(d, q, T, pool, pool, smap, k, ctx, None, out, None, small)
+    assert e.value.status == 4
+    host = torch.zeros((4, 8, 16, 128), dtype=torch.bfloat16)  # not pinned
+    with pytest.raises(ValueError):
+        P.oasis_build_summaries(d, host, torch.zeros((1, 16), dtype=torch.int32, device="cuda"), ctx,
+                                pool, pool)
+    with pytest.raises(P.OasisError) as e:
+        P.oasis_stage_blocks(d, host.pin_memory(), host.pin_memory(), torch.zeros((1, 16), dtype=torch.int32,
+                             device="cuda"), ctx, smap, torch.zeros((1, 8), dtype=torch.int32, device="cuda"), k,
+                             smap, smap.clone(), 0, k - 1, True, pool, pool, None,
+                             torch.empty(1 << 16, dtype=torch.uint8, device="cuda"))
+    assert e.value.status == 2  # capped eviction not implemented yet

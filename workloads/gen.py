@@ -314,3 +314,50 @@ def random_scores(seed: int, shape, n_distinct: int | None = None) -> np.ndarray
         vals = rng.standard_normal(n_distinct).astype(np.float32)
         return vals[rng.integers(0, n_distinct, size=shape)]
     return rng.standard_normal(shape).astype(np.float32) * np.float32(50.0)
+
+
+def random_bf16(seed: int, shape, scale: float = 1.0, mean: float = 0.0) -> np.ndarray:
+    """bf16 bits of N(mean, scale^2) values."""
+    x = _rng(seed).standard_normal(shape, dtype=np.float32) * np.float32(scale) + np.float32(mean)
+    return f32_to_bf16_bits(x)
+
+
+def random_selection(seed: int, n_cand, k: int, prev=None, keep_frac: float = 0.6):
+    """Ascending block-id selections [R][H][k] (-1 padded) and counts [R][H].
+
+    ``n_cand`` holds the candidate count of every request. With ``prev``, about
+    ``keep_frac`` of each previous selection is kept, which makes later staging
+    steps deltas rather than cold fills.
+    """
+    rng = _rng(seed)
+    n_cand = np.asarray(n_cand)
+    R = n_cand.shape[0]
+    H = prev[0].shape[1] if prev is not None else None
+    if H is None:
+        raise ValueError("pass prev=(sel, cnt) or use random_selection_h")
+    return _random_selection(rng, n_cand, H, k, prev, keep_frac)
+
+
+def random_selection_h(seed: int, n_cand, num_heads: int, k: int):
+    return _random_selection(_rng(seed), np.asarray(n_cand), num_heads, k, None, 0.0)
+
+
+def _random_selection(rng, n_cand, H, k, prev, keep_frac):
+    R = n_cand.shape[0]
+    sel = np.full((R, H, k), -1, np.int32)
+    cnt = np.zeros((R, H), np.int32)
+    for r in range(R):
+        nc = int(n_cand[r])
+        m = min(k, nc)
+        for h in range(H):
+            if prev is not None and m:
+                old = prev[0][r, h, :prev[1][r, h]]
+                keep = old[rng.random(old.size) < keep_frac] if old.size else old
+                rest = np.setdiff1d(np.arange(nc), keep)
+                extra = rng.choice(rest, size=m - min(m, keep.size), replace=False) if m > keep.size else []
+                chosen = np.sort(np.concatenate([keep[:m], np.asarray(extra, dtype=keep.dtype)]).astype(np.int32))
+            else:
+                chosen = np.sort(rng.choice(nc, size=m, replace=False)).astype(np.int32) if m else np.zeros(0, np.int32)
+            sel[r, h, :m] = chosen
+            cnt[r, h] = m
+    return sel, cnt

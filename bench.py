@@ -1,0 +1,305 @@
+"""Benchmark of the OasisKV decode-time hot path on one MI355X.
+
+One step = one pass of the whole path for one layer of a batch: attention of
+the stacked (verify + draft) queries over the HBM working set, and, on a
+background stream, block scoring from the draft queries, top-K selection and
+the delta staging of the selected blocks from the pinned host tier (paper
+§4.2.2 schedule for one layer). The value is decode steps per second per
+layer with every input resident in HBM (or in pinned host memory for the host
+tier) when the timed region starts.
+
+Workload (default): long-context serving, 8 requests x 131,072 tokens, GQA
+32 query / 8 KV heads, head_dim 128, block 16 (8,192 blocks), 4 draft tokens,
+2,048-token budget (K = 128 blocks + the local block), 1 % planted heavy-hitter
+blocks, queries following AR(1) over steps. Eight layer states rotate so that
+the working set of consecutive steps does not sit in the 256 MB Infinity Cache
+(the host K/V tier is shared by the layers; each layer has its own query
+stream, summaries, slot map and pools).
+
+Output: one JSON line (see the fields at the end of main()).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=40)
+    ap.add_argument("--workload", default="c4")
+    ap.add_argument("--budget", type=int, default=2048)
+    ap.add_argument("--layers", type=int, default=8, help="layer states rotated through (Infinity Cache defeat)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention comparison")
+    ap.add_argument("--isolated", action="store_true",
+                    help="also time score / top-K / attention alone (one stream, rotating layers)")
+    ap.add_argument("--copy-calib", action="store_true",
+                    help="only run a plain 1 GiB device copy (for scaling FETCH_SIZE/WRITE_SIZE counters)")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n, "dispatches": 3}), flush=True)
+
+
+def cpu_baseline(w, hk, hv, q0, k, budget_s):
+    """Time the oracle on a bounded sample: whole requests of the same workload."""
+    from oracle import oasis_oracle as O
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    import contextlib
+    c = w.cfg
+    ctx = w.ctx_len(0)
+    done, spent = 0, 0.0
+    limit = threadpool_limits(limits=1) if threadpool_limits is not None else contextlib.nullcontext()
+    with limit:
+        for r in range(c.num_reqs):
+            bt = w.block_table[r:r + 1]
+            cr = ctx[r:r + 1]
+            qr = q0[r:r + 1]
+            kmax, kmin = O.block_summaries(hk, bt, cr, c.block_size, w.NBmax)   # setup, not timed
+            t0 = time.perf_counter()
+            s = O.block_scores(qr, kmax, kmin, cr, c.num_kv_heads, c.block_size)
+            sel, cnt = O.select_topk(s, cr, k, c.block_size)
+            smap = np.full((1, c.num_kv_heads, k), -1, np.int32)
+            pk = np.zeros((1, k + 1, c.num_kv_heads, c.block_size, c.head_dim), np.uint16)
+            pv = np.zeros_like(pk)
+            O.stage_blocks(hk, hv, bt, sel, cnt, smap, np.zeros_like(smap), 0, pk, pv, cr, c.block_size)
+            O.sparse_attend(qr, pk, pv, smap, cr, c.block_size)
+            spent += time.perf_counter() - t0
+            done += 1
+            if spent >= budget_s:
+                break
+    per_step_s = spent / done * c.num_reqs
+    return {"value": 1.0 / per_step_s, "unit": "steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} of {c.num_reqs} requests (all {c.num_kv_heads} KV heads each): scores, top-K, "
+                      f"cold staging and attention in float64 NumPy on 1 thread, {spent:.1f} s, scaled to the "
+                      f"full batch"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures one GPU only; --gpus N with N > 1 is not supported "
+              "(the path has no cross-GPU step; see the sharding notes in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calib:
+        copy_calibration()
+        return
+
+    import torch
+
+    import paper_2608_08097_amd as P
+    from paper_2608_08097_amd.path import DecodePath, KernelTimer
+    from workloads import config, Workload
+
+    if not os.path.exists(P._lib.LIB_PATH):
+        from paper_2608_08097_amd.build_lib import build
+        build()
+    torch.cuda.set_device(0)
+
+    total_steps = args.warmup + args.steps
+    NL = max(1, args.layers)
+    per_layer_steps = (total_steps + NL - 1) // NL
+    cfg = config(args.workload, budget=args.budget, ar_queries=True, steps=per_layer_steps, grow_per_step=0)
+    w = Workload(cfg)
+    c = w.cfg
+    K = c.K
+    t0 = time.perf_counter()
+    shape = (w.NPhys, c.num_kv_heads, c.block_size, c.head_dim)
+    hk_t = torch.empty(shape, dtype=torch.int16, pin_memory=True)
+    hv_t = torch.empty(shape, dtype=torch.int16, pin_memory=True)
+    hk, hv = hk_t.numpy().view(np.uint16), hv_t.numpy().view(np.uint16)
+    w.fill_paged(hk, hv)
+    log(f"inputs: {c.name} R={c.num_reqs} L={list(w.ctx0[:2])}.. host KV {2 * hk.nbytes / 1e9:.2f} GB "
+        f"generated in {time.perf_counter() - t0:.1f} s")
+
+    d = P.dims(c.num_reqs, c.num_q_heads, c.num_kv_heads, c.head_dim, c.block_size, w.NBmax)
+    bt = torch.from_numpy(w.block_table).cuda()
+    ctx = w.ctx_len(0)
+    ctx_d = torch.from_numpy(ctx).cuda()
+    path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt)
+    layers = [path.new_layer() for _ in range(NL)]
+    path.build_summaries(layers[0], ctx_d)
+    for st in layers[1:]:
+        st.kmax.copy_(layers[0].kmax)
+        st.kmin.copy_(layers[0].kmin)
+    qs = [[torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16) for x in w.layer_queries(l, per_layer_steps)]
+          for l in range(NL)]
+    moved_log = torch.zeros((args.steps, c.num_reqs, c.num_kv_heads), dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+
+    timer = KernelTimer()
+
+    def run(i, timed):
+        l, s = i % NL, i // NL
+        path.step_pipelined(layers[l], qs[l][s], ctx_d, i, growing=False, timer=timer if timed else None,
+                            moved=moved_log[i - args.warmup] if timed else None)
+
+    for i in range(args.warmup):
+        run(i, False)
+    path.join()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} steps done")
+    t_start = time.perf_counter()
+    for i in range(args.warmup, total_steps):
+        run(i, True)
+    path.join()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms_per_step = 1000.0 * elapsed / args.steps
+    log(f"timed {args.steps} steps in {elapsed:.3f} s")
+
+    # per-kernel averages (HIP events on each kernel's stream)
+    us = {k_: timer.mean_us(k_) for k_ in ("score", "topk", "stage", "attn")}
+    n_cand = np.array([max(0, (int(L) + c.block_size - 1) // c.block_size - 1) for L in ctx])
+    bh = int(n_cand.sum()) * c.num_kv_heads                      # candidate block-heads per step
+    score_bytes = bh * (2 * c.head_dim * 2) + c.num_reqs * c.num_kv_heads * w.NBmax * 4 \
+        + c.num_reqs * c.T * c.num_q_heads * c.head_dim * 2
+    tok_per_head = K * c.block_size + np.array([L - c.block_size * nc for L, nc in zip(ctx, n_cand)])
+    attn_bytes = int(tok_per_head.sum()) * c.num_kv_heads * (2 * c.head_dim * 2) \
+        + 2 * c.num_reqs * c.T * c.num_q_heads * c.head_dim * 2
+    entry_bytes = 2 * c.block_size * c.head_dim * 2
+    moved = moved_log.cpu().numpy()
+    h2d_per_step = float(moved.sum()) / args.steps * entry_bytes
+    score_gbs = score_bytes / (us["score"] * 1e3)
+    attn_gbs = attn_bytes / (us["attn"] * 1e3)
+
+    dense = None
+    if not args.no_dense and args.workload == "c4":
+        dense = dense_attention(P, torch, w, hk_t, hv_t, ctx_d, d, c)
+
+    result = {
+        "metric": "sparse decode attn steps/s per layer + achieved HBM GB/s (% of peak) @2048 budget",
+        "value": round(1000.0 / ms_per_step, 2),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{c.name}: long-context serving, {c.num_reqs} requests x {int(ctx[0])} tokens, GQA "
+                        f"{c.num_q_heads}q/{c.num_kv_heads}kv, head_dim {c.head_dim}, block {c.block_size}, "
+                        f"{c.num_draft} draft tokens, budget {args.budget} (K={K}), AR(1) queries, "
+                        f"{NL} rotating layer states",
+            "global_batch": c.num_reqs, "seq_len": int(ctx[0]), "budget": args.budget, "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "score_kernel (oasis_score_blocks)",
+            "achieved": round(score_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(score_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "algorithmic_bytes": score_bytes, "avg_us": round(us["score"], 2),
+        },
+        "attention": {"avg_us": round(us["attn"], 2), "algorithmic_bytes": attn_bytes,
+                      "achieved_GBs": round(attn_gbs, 1), "frac": round(attn_gbs / HBM_PEAK_GBS, 4)},
+        "topk_us": round(us["topk"], 2),
+        "staging": {"avg_us": round(us["stage"], 2), "h2d_bytes_per_step": round(h2d_per_step),
+                    "entries_per_step": round(float(moved.sum()) / args.steps, 1),
+                    "h2d_GBs": round(h2d_per_step / (us["stage"] * 1e3), 2) if us["stage"] > 0 else None},
+        "dense_attention": dense,
+    }
+    if args.isolated:
+        result["isolated"] = isolated(P, torch, path, layers, qs, ctx_d, score_bytes, attn_bytes)
+    if not args.no_cpu_baseline:
+        q0 = w.layer_queries(0, 1)[0]
+        log("timing the oracle sample")
+        result["cpu_baseline"] = cpu_baseline(w, hk, hv, q0, K, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def isolated(P, torch, path, layers, qs, ctx_d, score_bytes, attn_bytes, iters=64):
+    """Each kernel alone on the current stream, rotating over the layer states."""
+    d, T, K = path.dims, path.T, path.k
+    NL = len(layers)
+    res = {}
+
+    def timeit(fn):
+        for i in range(8):
+            fn(layers[i % NL], qs[i % NL][0])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(iters):
+            fn(layers[i % NL], qs[i % NL][0])
+        e1.record()
+        torch.cuda.synchronize()
+        return 1000.0 * e0.elapsed_time(e1) / iters
+
+    us = timeit(lambda st, q: P.oasis_score_blocks(d, q, T, 1, T - 1, st.kmax, st.kmin, ctx_d, st.scores))
+    res["score"] = {"avg_us": round(us, 2), "GBs": round(score_bytes / (us * 1e3), 1)}
+    us = timeit(lambda st, q: P.oasis_select_topk(d, st.scores, ctx_d, K, st.sel, st.sel_count))
+    res["topk"] = {"avg_us": round(us, 2)}
+    us = timeit(lambda st, q: P.oasis_sparse_decode_attn(d, q, T, st.pool_k, st.pool_v, st.slot_map, K, ctx_d,
+                                                         None, st.out, st.lse, st.ws_attn))
+    res["attn"] = {"avg_us": round(us, 2), "GBs": round(attn_bytes / (us * 1e3), 1)}
+    return res
+
+
+def dense_attention(P, torch, w, hk_t, hv_t, ctx_d, d, c, iters=20):
+    """Same attention kernel over the whole context resident in HBM (identity slot map)."""
+    R, H, B, D = c.num_reqs, c.num_kv_heads, c.block_size, c.head_dim
+    nb = w.NBmax
+    bt = torch.from_numpy(w.block_table.astype(np.int64))
+    pool_k = torch.empty((R, nb, H, B, D), dtype=torch.bfloat16, device="cuda")
+    pool_v = torch.empty((R, nb, H, D, B), dtype=torch.bfloat16, device="cuda")
+    for r in range(R):
+        pages = bt[r]
+        pool_k[r].copy_(hk_t.view(torch.bfloat16)[pages].cuda())
+        pool_v[r].copy_(hv_t.view(torch.bfloat16)[pages].cuda().transpose(-1, -2))
+    ks = nb - 1
+    smap = torch.arange(ks, dtype=torch.int32, device="cuda").repeat(R * H).view(R, H, ks).contiguous()
+    out = torch.empty((R, c.T, c.num_q_heads, D), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((R, c.T, c.num_q_heads), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.oasis_attn_workspace_bytes(d, c.T, ks), dtype=torch.uint8, device="cuda")
+    q = torch.randn((R, c.T, c.num_q_heads, D), device="cuda").to(torch.bfloat16)
+    for _ in range(3):
+        P.oasis_sparse_decode_attn(d, q, c.T, pool_k, pool_v, smap, ks, ctx_d, None, out, lse, ws)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(iters):
+        P.oasis_sparse_decode_attn(d, q, c.T, pool_k, pool_v, smap, ks, ctx_d, None, out, lse, ws)
+    e1.record()
+    torch.cuda.synchronize()
+    us = 1000.0 * e0.elapsed_time(e1) / iters
+    nbytes = R * H * int(ctx_d[0].item()) * 2 * D * 2
+    del pool_k, pool_v
+    return {"avg_us": round(us, 2), "algorithmic_bytes": nbytes, "achieved_GBs": round(nbytes / (us * 1e3), 1),
+            "frac": round(nbytes / (us * 1e3) / HBM_PEAK_GBS, 4), "tokens_per_head": int(ctx_d[0].item())}
+
+
+if __name__ == "__main__":
+    main()

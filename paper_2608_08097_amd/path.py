@@ -50,6 +50,35 @@ class LayerState:
         self.slot_stamp.zero_()
 
 
+class KernelTimer:
+    """HIP events around library calls, recorded on the stream each call runs on."""
+
+    def __init__(self):
+        self.pairs: dict[str, list] = {}
+        self.enabled = True
+
+    def begin(self, name: str, stream):
+        if not self.enabled:
+            return None
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record(stream)
+        return ev
+
+    def end(self, name: str, stream, ev0):
+        if ev0 is None:
+            return
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev1.record(stream)
+        self.pairs.setdefault(name, []).append((ev0, ev1))
+
+    def mean_us(self, name: str) -> float:
+        ps = self.pairs.get(name, [])
+        return 1000.0 * sum(a.elapsed_time(b) for a, b in ps) / max(1, len(ps))
+
+    def reset(self):
+        self.pairs.clear()
+
+
 class DecodePath:
     """Issues score -> select -> stage -> attend for one layer on HIP streams.
 
@@ -105,7 +134,7 @@ class DecodePath:
         self.attend(st, q, ctx_len)
 
     def step_pipelined(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, step: int,
-                       growing: bool = False):
+                       growing: bool = False, timer: KernelTimer | None = None, moved: torch.Tensor | None = None):
         """One steady-state step (paper §4.2.2, one layer).
 
         Foreground (current stream): wait for this layer's previous transfer,
@@ -116,7 +145,10 @@ class DecodePath:
         With ``growing`` (one token appended per step) the local block is
         rewritten on the foreground before the attention, since it changes
         every step; otherwise the background stage refreshes it.
+        ``timer`` records HIP events around each call on its own stream;
+        ``moved`` (int32 [R][Hkv]) receives the entries this step copies.
         """
+        tm = timer if timer is not None else _NO_TIMER
         fg = torch.cuda.current_stream()
         bg = self.side
         ev_q = torch.cuda.Event()
@@ -126,15 +158,36 @@ class DecodePath:
             fg.wait_event(st.ev_staged)
         if growing:
             self.refresh_local(st, ctx_len, fg)
+        e = tm.begin("attn", fg)
         self.attend(st, q, ctx_len, fg)
+        tm.end("attn", fg, e)
         ev_attn = torch.cuda.Event()
         ev_attn.record(fg)
-        self.predict(st, q, ctx_len, bg)
+        e = tm.begin("score", bg)
+        L.oasis_score_blocks(self.dims, q, self.T, self.first_draft, self.num_draft, st.kmax, st.kmin, ctx_len,
+                             st.scores, bg)
+        tm.end("score", bg, e)
+        e = tm.begin("topk", bg)
+        L.oasis_select_topk(self.dims, st.scores, ctx_len, self.k, st.sel, st.sel_count, bg)
+        tm.end("topk", bg, e)
         bg.wait_event(ev_attn)  # the gather overwrites slots the attention reads
-        self.stage(st, ctx_len, step, bg, copy_local=not growing)
+        e = tm.begin("stage", bg)
+        L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, st.sel, st.sel_count,
+                             self.k, st.slot_map, st.slot_stamp, step, self.k, not growing, st.pool_k, st.pool_v,
+                             st.moved if moved is None else moved, st.ws_stage, bg)
+        tm.end("stage", bg, e)
         ev_staged = torch.cuda.Event()
         ev_staged.record(bg)
         st.ev_staged, st.ev_attended = ev_staged, ev_attn
 
     def join(self):
         torch.cuda.current_stream().wait_stream(self.side)
+
+
+class _NullTimer(KernelTimer):
+    def __init__(self):
+        super().__init__()
+        self.enabled = False
+
+
+_NO_TIMER = _NullTimer()

@@ -188,9 +188,25 @@ class Workload:
         return int((int(self.ctx0[r]) + B - 1) // B - 1)
 
     # -- queries ------------------------------------------------------------
-    def _eps(self, r: int, step: int) -> np.ndarray:
+    def _eps(self, r: int, step: int, layer: int = 0) -> np.ndarray:
         c = self.cfg
-        return _rng(c.base_seed + 2, r, step).standard_normal((c.T, c.num_q_heads, c.head_dim), dtype=np.float32)
+        key = (c.base_seed + 2, r, step) if layer == 0 else (c.base_seed + 2, r, step, layer)
+        return _rng(*key).standard_normal((c.T, c.num_q_heads, c.head_dim), dtype=np.float32)
+
+    def layer_queries(self, layer: int, steps: int) -> list[np.ndarray]:
+        """bf16 query bits of ``steps`` consecutive decode steps of one more layer.
+
+        Each layer has its own stream of draws; with ``ar_queries`` they follow
+        the same AR(1) recipe over steps.
+        """
+        c = self.cfg
+        state = np.stack([self._eps(r, 0, layer) for r in range(c.num_reqs)])
+        out = [f32_to_bf16_bits(state)]
+        for s in range(1, steps):
+            eps = np.stack([self._eps(r, s, layer) for r in range(c.num_reqs)])
+            state = (np.float32(0.9) * state + np.float32(0.436) * eps).astype(np.float32) if c.ar_queries else eps
+            out.append(f32_to_bf16_bits(state))
+        return out
 
     def queries_f32(self, step: int = 0) -> np.ndarray:
         """float32 query state [R][T][Hq][d] at ``step`` (before bf16 rounding)."""

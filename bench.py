@@ -130,7 +130,7 @@ def main():
 
     total_steps = args.warmup + args.steps
     NL = max(1, args.layers)
-    per_layer_steps = (total_steps + NL - 1) // NL
+    per_layer_steps = (total_steps + args.steps + NL - 1) // NL  # queries of both timed regions
     cfg = config(args.workload, budget=args.budget, ar_queries=True, steps=per_layer_steps, grow_per_step=0)
     w = Workload(cfg)
     c = w.cfg
@@ -161,24 +161,32 @@ def main():
 
     timer = KernelTimer()
 
-    def run(i, timed):
+    def run(i, timed, with_events):
         l, s = i % NL, i // NL
-        path.step_pipelined(layers[l], qs[l][s], ctx_d, i, growing=False, timer=timer if timed else None,
-                            moved=moved_log[i - args.warmup] if timed else None)
+        path.step_pipelined(layers[l], qs[l][s], ctx_d, i, growing=False, timer=timer if with_events else None,
+                            moved=moved_log[(i - args.warmup) % args.steps] if timed else None)
 
     for i in range(args.warmup):
-        run(i, False)
+        run(i, False, False)
     path.join()
     torch.cuda.synchronize()
     log(f"warmup {args.warmup} steps done")
+    # Timed region 1: the step rate (no events between kernels).
     t_start = time.perf_counter()
     for i in range(args.warmup, total_steps):
-        run(i, True)
+        run(i, True, False)
     path.join()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms_per_step = 1000.0 * elapsed / args.steps
     log(f"timed {args.steps} steps in {elapsed:.3f} s")
+    # Timed region 2: the same steps again with HIP events around every kernel,
+    # recorded on the stream the kernel runs on (per-kernel durations).
+    moved_rate = moved_log.cpu().numpy().copy()
+    for i in range(total_steps, total_steps + args.steps):
+        run(i, False, True)
+    path.join()
+    torch.cuda.synchronize()
 
     # per-kernel averages (HIP events on each kernel's stream)
     us = {k_: timer.mean_us(k_) for k_ in ("score", "topk", "stage", "attn")}
@@ -190,10 +198,10 @@ def main():
     attn_bytes = int(tok_per_head.sum()) * c.num_kv_heads * (2 * c.head_dim * 2) \
         + 2 * c.num_reqs * c.T * c.num_q_heads * c.head_dim * 2
     entry_bytes = 2 * c.block_size * c.head_dim * 2
-    moved = moved_log.cpu().numpy()
+    moved = moved_rate
     h2d_per_step = float(moved.sum()) / args.steps * entry_bytes
-    score_gbs = score_bytes / (us["score"] * 1e3)
-    attn_gbs = attn_bytes / (us["attn"] * 1e3)
+    score_gbs = score_bytes / (us["score"] * 1e3) if us["score"] > 0 else 0.0
+    attn_gbs = attn_bytes / (us["attn"] * 1e3) if us["attn"] > 0 else 0.0
 
     dense = None
     if not args.no_dense and args.workload == "c4":

@@ -15,8 +15,8 @@
  * General conventions
  * -------------------
  * - Every pointer is owned by the caller. The library allocates no memory; the
- *   scratch that a call needs is a caller-provided workspace whose size comes
- *   from the matching *_workspace_bytes function.
+ *   scratch the attention call needs is a caller-provided workspace whose
+ *   size comes from oasis_attn_workspace_bytes.
  * - Calls are asynchronous on `stream` (a hipStream_t passed as void*, NULL =
  *   the null stream). They return once the kernels are enqueued.
  * - Host-side checks (null pointers, supported sizes, workspace size) return
@@ -143,9 +143,6 @@ OASIS_API oasis_status oasis_score_blocks(const oasis_dims* dims, const uint16_t
 OASIS_API oasis_status oasis_select_topk(const oasis_dims* dims, const float* scores, const int32_t* ctx_len,
                                int32_t k, int32_t* sel, int32_t* sel_count, void* stream);
 
-/* Bytes of workspace oasis_stage_blocks needs for these sizes (0 if invalid). */
-OASIS_API size_t oasis_stage_workspace_bytes(const oasis_dims* dims, int32_t k);
-
 /*
  * Delta selection + KV transfer into the HBM working set (paper §4.2.3: resident
  * hits stay and move no bytes; non-selected residents are evicted least-recently-
@@ -167,8 +164,7 @@ OASIS_API size_t oasis_stage_workspace_bytes(const oasis_dims* dims, int32_t k);
  * and its victim slot is left free (-1).
  *
  * Local-only form: with sel == NULL and sel_count == NULL (and copy_local = 1)
- * only slot k is refreshed; slot_map, slot_stamp, moved and the workspace may
- * then be NULL. This stands in for the model writing the newest token's K/V
+ * only slot k is refreshed; slot_map, slot_stamp and moved may then be NULL. This stands in for the model writing the newest token's K/V
  * into the resident local block before attention.
  *
  * fetch_cap: most misses admitted per (r, h) per call; fetch_cap >= k means
@@ -184,7 +180,7 @@ OASIS_API oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t
                                 const int32_t* sel, const int32_t* sel_count, int32_t k,
                                 int32_t* slot_map, int32_t* slot_stamp, int32_t step, int32_t fetch_cap,
                                 int32_t copy_local, uint16_t* pool_k, uint16_t* pool_v, int32_t* moved,
-                                void* workspace, size_t workspace_bytes, void* stream);
+                                void* stream);
 
 /* Bytes of workspace oasis_sparse_decode_attn needs for these sizes (0 if invalid). */
 OASIS_API size_t oasis_attn_workspace_bytes(const oasis_dims* dims, int32_t num_q_tokens, int32_t k_slots);

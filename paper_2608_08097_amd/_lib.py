@@ -22,7 +22,7 @@ STATUS = {0: "OASIS_OK", 1: "OASIS_ERR_INVALID_ARG", 2: "OASIS_ERR_UNSUPPORTED",
 
 EXPORTS = (
     "oasis_last_error", "oasis_abi_version", "oasis_build_summaries", "oasis_score_blocks",
-    "oasis_select_topk", "oasis_stage_workspace_bytes", "oasis_stage_blocks",
+    "oasis_select_topk", "oasis_stage_blocks",
     "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn",
 )
 
@@ -74,11 +74,9 @@ def lib() -> ctypes.CDLL:
         L.oasis_score_blocks.argtypes = [_DIMS, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]
         L.oasis_select_topk.restype = _I32
         L.oasis_select_topk.argtypes = [_DIMS, _P, _P, _I32, _P, _P, _P]
-        L.oasis_stage_workspace_bytes.restype = _SZ
-        L.oasis_stage_workspace_bytes.argtypes = [_DIMS, _I32]
         L.oasis_stage_blocks.restype = _I32
         L.oasis_stage_blocks.argtypes = [_DIMS, _P, _P, _I64, _P, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
-                                         _P, _P, _P, _P, _SZ, _P]
+                                         _P, _P, _P, _P]
         L.oasis_attn_workspace_bytes.restype = _SZ
         L.oasis_attn_workspace_bytes.argtypes = [_DIMS, _I32, _I32]
         L.oasis_sparse_decode_attn.restype = _I32
@@ -182,13 +180,9 @@ def oasis_select_topk(d: OasisDims, scores, ctx_len, k: int, sel, sel_count, str
         _dev(sel, "sel", _I32T), _dev(sel_count, "sel_count", _I32T), _stream(stream)))
 
 
-def oasis_stage_workspace_bytes(d: OasisDims, k: int) -> int:
-    return int(lib().oasis_stage_workspace_bytes(ctypes.byref(d), int(k)))
-
-
 def oasis_stage_blocks(d: OasisDims, host_k, host_v, host_block_table, ctx_len, sel, sel_count, k: int,
                        slot_map, slot_stamp, step: int, fetch_cap: int, copy_local: bool, pool_k, pool_v,
-                       moved, workspace, stream=None) -> None:
+                       moved, stream=None) -> None:
     if host_k.shape != host_v.shape:
         raise ValueError("host_k and host_v differ in shape")
     R, H, B, D = d.num_reqs, d.num_kv_heads, d.block_size, d.head_dim
@@ -207,9 +201,7 @@ def oasis_stage_blocks(d: OasisDims, host_k, host_v, host_block_table, ctx_len, 
         _dev(sel, "sel", _I32T, nullable=True), _dev(sel_count, "sel_count", _I32T, nullable=True), int(k),
         _dev(slot_map, "slot_map", _I32T, nullable=True), _dev(slot_stamp, "slot_stamp", _I32T, nullable=True),
         int(step), int(fetch_cap), 1 if copy_local else 0, _dev(pool_k, "pool_k", _BF16),
-        _dev(pool_v, "pool_v", _BF16), _dev(moved, "moved", _I32T, nullable=True),
-        _dev(workspace, "workspace", (torch.uint8,), nullable=True),
-        0 if workspace is None else int(workspace.numel()), _stream(stream)))
+        _dev(pool_v, "pool_v", _BF16), _dev(moved, "moved", _I32T, nullable=True), _stream(stream)))
 
 
 def oasis_attn_workspace_bytes(d: OasisDims, num_q_tokens: int, k_slots: int) -> int:

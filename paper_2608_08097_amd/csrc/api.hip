@@ -141,17 +141,11 @@ oasis_status oasis_select_topk(const oasis_dims* dims, const float* scores, cons
   return hip_status(oasis::launch_topk(a, static_cast<hipStream_t>(stream)), fn);
 }
 
-size_t oasis_stage_workspace_bytes(const oasis_dims* dims, int32_t k) {
-  if (check_dims(dims, "oasis_stage_workspace_bytes") != OASIS_OK || k < 1 || k > 1024) return 0;
-  return oasis::stage_workspace_bytes(dims->num_reqs, dims->num_kv_heads, k);
-}
-
 oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, const uint16_t* host_v,
                                 int64_t num_pages, const int32_t* host_block_table, const int32_t* ctx_len,
                                 const int32_t* sel, const int32_t* sel_count, int32_t k, int32_t* slot_map,
                                 int32_t* slot_stamp, int32_t step, int32_t fetch_cap, int32_t copy_local,
-                                uint16_t* pool_k, uint16_t* pool_v, int32_t* moved, void* workspace,
-                                size_t workspace_bytes, void* stream) {
+                                uint16_t* pool_k, uint16_t* pool_v, int32_t* moved, void* stream) {
   static const char* fn = "oasis_stage_blocks";
   oasis_status st = check_dims(dims, fn);
   if (st != OASIS_OK) return st;
@@ -176,14 +170,10 @@ oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, 
   if (!local_only) {
     REQUIRE_PTR(slot_map, fn);
     REQUIRE_PTR(slot_stamp, fn);
-    const size_t need = oasis::stage_workspace_bytes(dims->num_reqs, dims->num_kv_heads, k);
-    if (!workspace || workspace_bytes < need)
-      return fail(OASIS_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, workspace_bytes, need);
   }
   const void *hk = nullptr, *hv = nullptr;
   if ((st = device_view(host_k, &hk, "host_k", fn)) != OASIS_OK) return st;
   if ((st = device_view(host_v, &hv, "host_v", fn)) != OASIS_OK) return st;
-  const size_t nrh = (size_t)dims->num_reqs * dims->num_kv_heads;
   oasis::StageArgs a{};
   a.host_k = static_cast<const uint16_t*>(hk);
   a.host_v = static_cast<const uint16_t*>(hv);
@@ -197,8 +187,6 @@ oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, 
   a.pool_k = pool_k;
   a.pool_v = pool_v;
   a.moved = moved;
-  a.plan = local_only ? nullptr : static_cast<int32_t*>(workspace);
-  a.plan_count = local_only ? nullptr : static_cast<int32_t*>(workspace) + nrh * (size_t)k * 2;
   a.local_only = local_only ? 1 : 0;
   a.R = dims->num_reqs;
   a.Hkv = dims->num_kv_heads;

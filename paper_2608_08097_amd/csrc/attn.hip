@@ -30,8 +30,12 @@ namespace oasis {
 
 namespace {
 
-constexpr int kW = 4;                 // waves per workgroup
+constexpr int kW = 4;  // waves per workgroup
+// Workgroups of one attention call: one per CU when the kernel prefetches
+// (one wave per SIMD), two otherwise.
+constexpr int kTargetWorkgroupsPrefetch = 256;
 constexpr int kTargetWorkgroups = 512;
+constexpr int kMaxSplits = 16;
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -47,9 +51,163 @@ __device__ __forceinline__ bool map_workgroup(int wg, int nrh, int nsplit, int& 
   return rh < nrh;
 }
 
+// K and V registers of one 32-token unit, plus the token counts of its two
+// slots (0 = not attended).
+struct UnitRegs {
+  u32x4 k[2][4];
+  u32x4 v[8];
+  int n0, n1;
+};
+
+template <int BS>
+__device__ __forceinline__ void load_unit(UnitRegs& ur, int u, int ks, int local_len, const int32_t* smap,
+                                          const uint16_t* pk, const uint16_t* pv, long long slot_elems, int g,
+                                          int i) {
+  // u is wave-uniform. Every slot <= ks lies inside the pool, so the K/V loads
+  // are issued without waiting for the slot map; its entries only decide
+  // afterwards which tokens count (free slots may hold anything, even NaN).
+  int s0, s1;
+  if (BS == 16) {
+    s0 = 2 * u;
+    s1 = 2 * u + 1;
+  } else {
+    s0 = u;
+    s1 = ks + 1;
+  }
+  const bool in0 = s0 <= ks, in1 = s1 <= ks;
+  // K: lane (g, i), token tile tau -> unit token 8*(i/4) + 4*tau + i%4
+#pragma unroll
+  for (int tau = 0; tau < 2; ++tau) {
+    const int tok = 8 * (i >> 2) + 4 * tau + (i & 3);
+    int slot, row;
+    bool in;
+    if (BS == 16) {
+      slot = tok < 16 ? s0 : s1;
+      row = tok & 15;
+      in = tok < 16 ? in0 : in1;
+    } else {
+      slot = s0;
+      row = tok;
+      in = in0;
+    }
+    const uint16_t* src = pk + (long long)(in ? slot : 0) * slot_elems + row * kHeadDim + g * 8;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) ur.k[tau][st] = in ? ldg16(src + st * 32) : u32x4{0, 0, 0, 0};
+  }
+  // V^T: lane (g, i), d-tile dt -> V[tokens 8g .. 8g+7][d = dt*16 + i]
+  int vslot, t0;
+  bool vin;
+  if (BS == 16) {
+    vslot = g < 2 ? s0 : s1;
+    t0 = (g & 1) * 8;
+    vin = g < 2 ? in0 : in1;
+  } else {
+    vslot = s0;
+    t0 = 8 * g;
+    vin = in0;
+  }
+  const uint16_t* src = pv + (long long)(vin ? vslot : 0) * slot_elems + t0;
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) ur.v[dt] = vin ? ldg16(src + (long long)(dt * 16 + i) * BS) : u32x4{0, 0, 0, 0};
+  // token counts of the two slots (0 = not attended)
+  const int n0 = s0 < ks ? (smap[s0] >= 0 ? BS : 0) : (s0 == ks ? local_len : 0);
+  int n1 = 0;
+  if (BS == 16) n1 = s1 < ks ? (smap[s1] >= 0 ? BS : 0) : (s1 == ks ? local_len : 0);
+  ur.n0 = n0;
+  ur.n1 = n1;
+}
+
+// Zero the V values of tokens that are not attended (their probability is 0,
+// but 0 * NaN would poison the accumulator).
+template <int BS>
+__device__ __forceinline__ void mask_unit_v(UnitRegs& ur, int g) {
+  const int cnt = BS == 16 ? (g < 2 ? ur.n0 : ur.n1) : ur.n0;
+  const int t0 = BS == 16 ? (g & 1) * 8 : 8 * g;
+  const int keep = cnt - t0;
+  if (keep >= 8) return;
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const uint32_t lo = (2 * w) < keep ? 0x0000FFFFu : 0u;
+      const uint32_t hi = (2 * w + 1) < keep ? 0xFFFF0000u : 0u;
+      ur.v[dt][w] &= (lo | hi);
+    }
+}
+
+// Online-softmax update of one wave with one 32-token unit (all row tiles).
+//
+// Lazy rescaling: every row keeps a reference maximum m_ref (the same in the
+// four lanes of the row) and each lane a partial sum over its own tokens.
+// Probabilities are exp2(x - m_ref); only when some score of the wave exceeds
+// its row reference by more than kLazyTh (a wave-uniform branch, rare once the
+// first unit has been seen) are the row maxima exchanged across lanes and the
+// accumulators rescaled. Probabilities stay below 2^kLazyTh, far inside the
+// fp32 range, and the result is the same softmax.
+constexpr float kLazyTh = 8.f;
+
+template <int NT, int BS>
+__device__ __forceinline__ void process_unit(const UnitRegs& cur, const bf16x8 (&qb)[NT][4], float (&m_ref)[NT],
+                                             float (&l_part)[NT], f32x4 (&acc)[NT][8], int g, float scale_log2) {
+  // validity of the 8 unit tokens 8g + 4*tau + j this lane scores
+  bool valid[2][4];
+#pragma unroll
+  for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int tok = 8 * g + 4 * tau + j;
+      valid[tau][j] = BS == 16 ? (tok < 16 ? tok < cur.n0 : (tok - 16) < cur.n1) : tok < cur.n0;
+    }
+#pragma unroll
+  for (int v = 0; v < NT; ++v) {
+    f32x4 sc[2];
+#pragma unroll
+    for (int tau = 0; tau < 2; ++tau) {
+      f32x4 s4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+        s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cur.k[tau][st]), qb[v][st], s4, 0, 0, 0);
+      sc[tau] = s4;
+    }
+    float x[8];
+    float lmax = -INFINITY;
+#pragma unroll
+    for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float z = valid[tau][j] ? sc[tau][j] * scale_log2 : -INFINITY;
+        x[4 * tau + j] = z;
+        lmax = fmaxf(lmax, z);
+      }
+    if (__builtin_amdgcn_ballot_w64(lmax > m_ref[v] + kLazyTh)) {
+      float rmax = fmaxf(lmax, __shfl_xor(lmax, 16));
+      rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
+      const float m_new = fmaxf(m_ref[v], rmax);
+      const float alpha = m_new == -INFINITY ? 1.f : fast_exp2(m_ref[v] - m_new);
+      l_part[v] *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) acc[v][dt] *= alpha;
+      m_ref[v] = m_new;
+    }
+    const float m_use = m_ref[v] == -INFINITY ? 0.f : m_ref[v];
+    bf16x8 pb;
+    float psum = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float pe = fast_exp2(x[e] - m_use);
+      psum += pe;
+      pb[e] = (__bf16)pe;
+    }
+    l_part[v] += psum;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt)
+      acc[v][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(cur.v[dt]), pb, acc[v][dt], 0, 0, 0);
+  }
+}
+
 template <int NT, int BS>
 __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
   const int i = lane & 15;
@@ -61,7 +219,7 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   const Ctx c = ctx_blocks(a.ctx_len[r], BS, a.NBmax);
   const int ks = a.k_slots;
 
-  // Q^T operand: lane (g, i) holds row i of tile v, dims st*32 + 8g .. +8.
+  // Q^T operand: lane (g, i) holds row v*16 + i of tile v, dims st*32 + 8g .. +8.
   bf16x8 qb[NT][4];
 #pragma unroll
   for (int v = 0; v < NT; ++v) {
@@ -84,7 +242,7 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   const uint16_t* pv = a.pool_v + (long long)r * (ks + 1) * slot_elems + head_off;
   const int32_t* smap = a.slot_map + (long long)rh * ks;
 
-  float m_run[NT], l_run[NT];
+  float m_run[NT], l_run[NT];  // row reference maximum (log2 units) and this lane's partial sum
   f32x4 acc[NT][8];
 #pragma unroll
   for (int v = 0; v < NT; ++v) {
@@ -96,127 +254,34 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
 
   const int u_begin = split * a.units_per_split;
   const int u_end = min(a.n_units, u_begin + a.units_per_split);
-  for (int u = u_begin + wave; u < u_end; u += kW) {
-    // slots of this unit and their token counts (0 = not attended)
-    int s0, s1, n0, n1;
-    if (BS == 16) {
-      s0 = 2 * u;
-      s1 = 2 * u + 1;
-    } else {
-      s0 = u;
-      s1 = -1;
-    }
-    n0 = s0 < ks ? (smap[s0] >= 0 ? BS : 0) : (s0 == ks ? c.local_len : 0);
-    n1 = 0;
-    if (BS == 16) n1 = s1 < ks ? (smap[s1] >= 0 ? BS : 0) : (s1 == ks ? c.local_len : 0);
 
-    // K: lane (g, i), token tile tau -> unit token 8*(i/4) + 4*tau + i%4
-    u32x4 kr[2][4];
-#pragma unroll
-    for (int tau = 0; tau < 2; ++tau) {
-      const int tok = 8 * (i >> 2) + 4 * tau + (i & 3);
-      int slot, row, cnt;
-      if (BS == 16) {
-        slot = tok < 16 ? s0 : s1;
-        row = tok & 15;
-        cnt = tok < 16 ? n0 : n1;
-      } else {
-        slot = s0;
-        row = tok;
-        cnt = n0;
-      }
-      const bool live = row < cnt;
-      const uint16_t* src = pk + (long long)slot * slot_elems + row * kHeadDim + g * 8;
-#pragma unroll
-      for (int st = 0; st < 4; ++st) kr[tau][st] = live ? ldg16(src + st * 32) : u32x4{0, 0, 0, 0};
+  // With few row tiles the next unit's K/V loads are issued before the current
+  // unit is computed (one exposed memory latency per wave, not per unit); with
+  // many row tiles the registers go to the accumulators instead.
+  constexpr bool kPrefetch = NT <= 2;
+  int u = u_begin + wave;
+  if (kPrefetch) {
+    UnitRegs cur, nxt;
+    if (u < u_end) load_unit<BS>(cur, u, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
+    for (; u < u_end; u += kW) {
+      if (u + kW < u_end) load_unit<BS>(nxt, u + kW, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
+      mask_unit_v<BS>(cur, g);
+      process_unit<NT, BS>(cur, qb, m_run, l_run, acc, g, a.scale_log2);
+      cur = nxt;
     }
-    // V^T: lane (g, i), d-tile dt -> V[tokens 8g .. 8g+7][d = dt*16 + i]
-    u32x4 vr[8];
-    {
-      int slot, t0, cnt;
-      if (BS == 16) {
-        slot = g < 2 ? s0 : s1;
-        t0 = (g & 1) * 8;
-        cnt = g < 2 ? n0 : n1;
-      } else {
-        slot = s0;
-        t0 = 8 * g;
-        cnt = n0;
-      }
-      const bool live = t0 < cnt;
-      const uint16_t* src = pv + (long long)slot * slot_elems + t0;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) vr[dt] = live ? ldg16(src + (long long)(dt * 16 + i) * BS) : u32x4{0, 0, 0, 0};
-      if (live && cnt - t0 < 8) {  // partial local block: clear the tokens past its end
-        const int keep = cnt - t0;
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt)
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const uint32_t lo = (2 * w) < keep ? 0x0000FFFFu : 0u;
-            const uint32_t hi = (2 * w + 1) < keep ? 0xFFFF0000u : 0u;
-            vr[dt][w] &= (lo | hi);
-          }
-      }
+  } else {
+    for (; u < u_end; u += kW) {
+      UnitRegs cur;
+      load_unit<BS>(cur, u, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
+      mask_unit_v<BS>(cur, g);
+      process_unit<NT, BS>(cur, qb, m_run, l_run, acc, g, a.scale_log2);
     }
-
-    // validity of the 8 unit tokens 8g + 4*tau + j this lane scores
-    bool valid[2][4];
+  }
+  // row sums: add the partial sums of the four lanes of every row
 #pragma unroll
-    for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int tok = 8 * g + 4 * tau + j;
-        valid[tau][j] = BS == 16 ? (tok < 16 ? tok < n0 : (tok - 16) < n1) : tok < n0;
-      }
-
-#pragma unroll
-    for (int v = 0; v < NT; ++v) {
-      f32x4 sc[2];
-#pragma unroll
-      for (int tau = 0; tau < 2; ++tau) {
-        f32x4 s4 = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-          s4 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kr[tau][st]), qb[v][st], s4, 0, 0, 0);
-        sc[tau] = s4;
-      }
-      float x[8];
-      float mx = -INFINITY;
-#pragma unroll
-      for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float z = valid[tau][j] ? sc[tau][j] * a.scale_log2 : -INFINITY;
-          x[4 * tau + j] = z;
-          mx = fmaxf(mx, z);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m_run[v], mx);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float alpha = fast_exp2(m_run[v] - m_use);
-      float p[8];
-      float psum = 0.f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        p[e] = fast_exp2(x[e] - m_use);
-        psum += p[e];
-      }
-      psum += __shfl_xor(psum, 16);
-      psum += __shfl_xor(psum, 32);
-      l_run[v] = l_run[v] * alpha + psum;
-      m_run[v] = m_new;
-      u32x4 pk4;
-#pragma unroll
-      for (int w = 0; w < 4; ++w) pk4[w] = f32_to_bf16_bits(p[2 * w]) | (f32_to_bf16_bits(p[2 * w + 1]) << 16);
-      const bf16x8 pb = as_bf16x8(pk4);
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        acc[v][dt] *= alpha;
-        acc[v][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vr[dt]), pb, acc[v][dt], 0, 0, 0);
-      }
-    }
+  for (int v = 0; v < NT; ++v) {
+    l_run[v] += __shfl_xor(l_run[v], 16);
+    l_run[v] += __shfl_xor(l_run[v], 32);
   }
 
   // ---- merge the waves of this workgroup through LDS -----------------------
@@ -288,7 +353,8 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   }
 }
 
-// One workgroup per (row, request x KV head); one thread per dimension.
+// One workgroup per (row, request x KV head); one thread per dimension. All
+// partial loads of a thread are issued before any is used (nsplit <= kMaxSplits).
 __global__ __launch_bounds__(kHeadDim) void attn_merge_kernel(AttnArgs a) {
   const int row = blockIdx.x;
   const int rh = blockIdx.y;
@@ -296,17 +362,25 @@ __global__ __launch_bounds__(kHeadDim) void attn_merge_kernel(AttnArgs a) {
   const int r = rh / a.Hkv;
   const int h = rh - r * a.Hkv;
   const long long base = (long long)rh * a.nsplit * a.rows + row;
+  float ms[kMaxSplits], ls[kMaxSplits], os[kMaxSplits];
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s) {
+    const long long idx = base + (long long)s * a.rows;
+    const bool live = s < a.nsplit;
+    ms[s] = live ? a.part_ml[idx * 2] : -INFINITY;
+    ls[s] = live ? a.part_ml[idx * 2 + 1] : 0.f;
+    os[s] = live ? a.part_o[idx * kHeadDim + d] : 0.f;
+  }
   float M = -INFINITY;
-  for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, a.part_ml[(base + (long long)s * a.rows) * 2]);
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s) M = fmaxf(M, ms[s]);
   float L = 0.f, o = 0.f;
   if (M != -INFINITY) {
-    for (int s = 0; s < a.nsplit; ++s) {
-      const long long idx = base + (long long)s * a.rows;
-      const float ms = a.part_ml[idx * 2];
-      if (ms == -INFINITY) continue;
-      const float f = fast_exp2(ms - M);
-      L += a.part_ml[idx * 2 + 1] * f;
-      o += a.part_o[idx * kHeadDim + d] * f;
+#pragma unroll
+    for (int s = 0; s < kMaxSplits; ++s) {
+      const float f = ms[s] == -INFINITY ? 0.f : fast_exp2(ms[s] - M);
+      L += ls[s] * f;
+      o += os[s] * f;
     }
   }
   const float res = L > 0.f ? o / L : 0.f;
@@ -348,9 +422,11 @@ AttnPlan attn_plan(int R, int Hq, int Hkv, int T, int B, int k_slots) {
   p.rows = G * T;
   p.n_units = B == 16 ? (k_slots + 2) / 2 : k_slots + 1;
   const long long nrh = (long long)R * Hkv;
-  long long want = (kTargetWorkgroups + nrh - 1) / (nrh > 0 ? nrh : 1);
+  const int target = (p.rows + 15) / 16 <= 2 ? kTargetWorkgroupsPrefetch : kTargetWorkgroups;
+  long long want = (target + nrh - 1) / (nrh > 0 ? nrh : 1);
   const long long most = (p.n_units + kW - 1) / kW;  // at least one unit per wave
   if (want > most) want = most;
+  if (want > kMaxSplits) want = kMaxSplits;
   if (want < 1) want = 1;
   p.units_per_split = (int)((p.n_units + want - 1) / want);
   p.nsplit = (p.n_units + p.units_per_split - 1) / p.units_per_split;

@@ -89,12 +89,9 @@ struct StageArgs {
   uint16_t* pool_k;
   uint16_t* pool_v;
   int32_t* moved;
-  int32_t* plan;            // workspace: [R*Hkv][k] (slot, page) pairs
-  int32_t* plan_count;      // workspace: [R*Hkv]
   int R, Hkv, B, NBmax, k, step, copy_local;
   int local_only;           // no selection: refresh the local block only
 };
-size_t stage_workspace_bytes(int R, int Hkv, int k);
 hipError_t launch_stage(const StageArgs& a, hipStream_t s);
 
 struct AttnArgs {

@@ -8,15 +8,22 @@
 // the selected block-head entries from pinned host memory over PCIe and
 // writes them into the resident GPU pages.
 //
-// plan kernel   one 256-thread workgroup per (request, KV head); the slot map,
-//               stamps and selection sit in LDS; ranks come from block scans
-//               (free slots, misses) and from counting (stale slots by
-//               (stamp, slot)). It updates slot_map / slot_stamp in place and
-//               writes (slot, page) pairs to the workspace.
-// gather kernel one 256-thread workgroup per planned entry (plus one per head
-//               for the local block): 16-byte loads from the host page (PCIe),
-//               K stored token-major, V transposed through LDS to the d x B
-//               layout the attention kernel consumes.
+// A small fixed grid of 256-thread workgroups walks the (request, KV head)
+// pairs (workgroup w takes pairs w, w + grid, ...); for each pair it does:
+//   plan   the slot map, stamps and selection sit in LDS; ranks come from
+//          workgroup scans (free slots, misses) and from counting (stale
+//          slots by (stamp, slot)); slot_map / slot_stamp are updated in place
+//          and the (slot, page) pairs stay in LDS;
+//   copy   the entries are streamed in batches of PF: the PCIe loads of a
+//          whole batch (PF x 2 x B x d x 2 bytes) are issued before any is
+//          stored, K goes to the pool token-major, V is transposed through LDS
+//          into the d x B layout the attention kernel reads.
+// Host reads wait microseconds in the memory system, and while they are
+// outstanding they slow the HBM traffic of every concurrent kernel (measured
+// on MI355X: 64 copying workgroups triple the duration of a concurrent block
+// scan, 16 add about 20 %, and 16 x 8 KiB in flight already saturate the
+// link). So the grid holds at most kCopyWorkgroups workgroups with about
+// kCopyInflight entries in flight between them.
 #include <climits>
 
 #include "oasis_internal.h"
@@ -28,11 +35,8 @@ namespace {
 constexpr int kPlanThreads = 256;
 constexpr int kMaxK = 1024;
 constexpr int kPer = kMaxK / kPlanThreads;  // items per thread in the scans
-
-struct PlanEntry {
-  int32_t slot;
-  int32_t page;
-};
+constexpr int kCopyWorkgroups = 16;
+constexpr int kCopyInflight = 16;  // block-head entries (K and V) in flight over the whole grid
 
 __device__ int wg_exclusive_scan(int v, int* s_wave) {
   const int lane = threadIdx.x & 63;
@@ -55,13 +59,11 @@ __device__ int wg_exclusive_scan(int v, int* s_wave) {
   return base + x - v;
 }
 
-__global__ __launch_bounds__(kPlanThreads) void stage_plan_kernel(StageArgs a) {
-  const int rh = blockIdx.x;
-  const int r = rh / a.Hkv;
+// Plan of one (request, KV head); returns the number of entries in s_slot/s_page.
+__device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int* s_page, int* s_wave) {
   const int tid = threadIdx.x;
   const int k = a.k;
   __shared__ int s_sel[kMaxK], s_map[kMaxK], s_stamp[kMaxK], s_hit[kMaxK], s_keep[kMaxK], s_vict[kMaxK];
-  __shared__ int s_wave[8];
 
   const long long base = (long long)rh * k;
   int m = a.sel_count[rh];
@@ -131,7 +133,6 @@ __global__ __launch_bounds__(kPlanThreads) void stage_plan_kernel(StageArgs a) {
   __syncthreads();
 
   // pair the i-th miss with the i-th victim
-  PlanEntry* plan = reinterpret_cast<PlanEntry*>(a.plan) + base;
   int moved_local = 0;
   {
     int mr = miss_base;
@@ -145,7 +146,8 @@ __global__ __launch_bounds__(kPlanThreads) void stage_plan_kernel(StageArgs a) {
       int page = -1;
       if (v >= 0 && blk >= 0 && blk < a.NBmax) page = a.block_table[(long long)r * a.NBmax + blk];
       if (page < 0 || page >= a.num_pages) page = -1;
-      plan[mr] = PlanEntry{v, page};
+      s_slot[mr] = v;
+      s_page[mr] = page;
       if (v >= 0) {
         s_map[v] = page >= 0 ? blk : -1;
         s_keep[v] = page >= 0;
@@ -154,7 +156,6 @@ __global__ __launch_bounds__(kPlanThreads) void stage_plan_kernel(StageArgs a) {
       ++mr;
     }
   }
-  // total copied entries (reuses the scan's total)
   wg_exclusive_scan(moved_local, s_wave);
   const int moved = s_wave[4];
 
@@ -162,83 +163,112 @@ __global__ __launch_bounds__(kPlanThreads) void stage_plan_kernel(StageArgs a) {
     a.slot_map[base + s] = s_map[s];
     if (s_keep[s]) a.slot_stamp[base + s] = a.step;
   }
-  if (tid == 0) {
-    a.plan_count[rh] = n_miss;
-    if (a.moved) a.moved[rh] = moved;
-  }
+  if (tid == 0 && a.moved) a.moved[rh] = moved;
+  return n_miss;
 }
 
-template <int BS>
-__global__ __launch_bounds__(256) void stage_gather_kernel(StageArgs a) {
-  const int rh = blockIdx.y;
-  const int e = a.local_only ? a.k : (int)blockIdx.x;
+template <int BS, int PF>
+__global__ __launch_bounds__(kPlanThreads) void stage_kernel(StageArgs a) {
+  const int tid = threadIdx.x;
+  __shared__ int s_slot[kMaxK + 1], s_page[kMaxK + 1];
+  __shared__ int s_wave[8];
+  constexpr int kElems = BS * kHeadDim;          // one K (or V) block-head entry
+  constexpr int kChunks = kElems / 8 / kPlanThreads;  // 16-byte chunks per thread
+  __shared__ uint16_t tile[PF][kElems];
+
+  for (int rh = blockIdx.x; rh < a.R * a.Hkv; rh += gridDim.x) {
   const int r = rh / a.Hkv;
   const int h = rh - r * a.Hkv;
-  const int tid = threadIdx.x;
-  int slot, page;
-  if (e < a.k) {
-    if (e >= a.plan_count[rh]) return;
-    const PlanEntry p = reinterpret_cast<const PlanEntry*>(a.plan)[(long long)rh * a.k + e];
-    slot = p.slot;
-    page = p.page;
-    if (page < 0 || slot < 0 || slot >= a.k) return;
-  } else {
-    if (!a.copy_local) return;
+  int n = a.local_only ? 0 : plan_entries(a, rh, r, s_slot, s_page, s_wave);
+  if (a.copy_local) {
     const Ctx c = ctx_blocks(a.ctx_len[r], BS, a.NBmax);
-    if (c.nb == 0) return;
-    page = a.block_table[(long long)r * a.NBmax + c.nb - 1];
-    if (page < 0 || page >= a.num_pages) return;
-    slot = a.k;
-  }
-  constexpr int kElems = BS * kHeadDim;
-  const long long src = ((long long)page * a.Hkv + h) * kElems;
-  const long long dst = (((long long)r * (a.k + 1) + slot) * a.Hkv + h) * kElems;
-  __shared__ uint16_t tile[kElems];
-#pragma unroll
-  for (int c = tid; c < kElems / 8; c += 256) {
-    const u32x4 kv = ldg16(a.host_k + src + c * 8);
-    const u32x4 vv = ldg16(a.host_v + src + c * 8);
-    *reinterpret_cast<u32x4*>(a.pool_k + dst + c * 8) = kv;
-    *reinterpret_cast<u32x4*>(tile + c * 8) = vv;
+    if (c.nb > 0) {
+      const int page = a.block_table[(long long)r * a.NBmax + c.nb - 1];
+      if (tid == 0) {
+        s_slot[n] = a.k;
+        s_page[n] = (page >= 0 && page < a.num_pages) ? page : -1;
+      }
+      ++n;
+    }
   }
   __syncthreads();
-  // V: [BS][d] -> [d][BS]; thread -> (d, 8-token group)
-  constexpr int kGroups = BS / 8;
+
+  for (int e0 = 0; e0 < n; e0 += PF) {
+    u32x4 kr[PF][kChunks], vr[PF][kChunks];
+    int slot[PF], page[PF];
 #pragma unroll
-  for (int w = tid; w < kHeadDim * kGroups; w += 256) {
-    const int d = w / kGroups;
-    const int t0 = (w % kGroups) * 8;
-    u32x4 o;
+    for (int p = 0; p < PF; ++p) {
+      const int e = e0 + p;
+      slot[p] = e < n ? s_slot[e] : -1;
+      page[p] = e < n ? s_page[e] : -1;
+      const bool live = page[p] >= 0 && slot[p] >= 0 && slot[p] <= a.k;
+      if (!live) page[p] = -1;
+      const long long src = ((long long)(live ? page[p] : 0) * a.Hkv + h) * kElems;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint32_t lo = tile[(t0 + 2 * j) * kHeadDim + d];
-      const uint32_t hi = tile[(t0 + 2 * j + 1) * kHeadDim + d];
-      o[j] = lo | (hi << 16);
+      for (int q = 0; q < kChunks; ++q) {
+        const int c = (q * kPlanThreads + tid) * 8;
+        kr[p][q] = live ? ldg16(a.host_k + src + c) : u32x4{0, 0, 0, 0};
+        vr[p][q] = live ? ldg16(a.host_v + src + c) : u32x4{0, 0, 0, 0};
+      }
     }
-    *reinterpret_cast<u32x4*>(a.pool_v + dst + (long long)d * BS + t0) = o;
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+      if (page[p] < 0) continue;
+      const long long dst = (((long long)r * (a.k + 1) + slot[p]) * a.Hkv + h) * kElems;
+#pragma unroll
+      for (int q = 0; q < kChunks; ++q) {
+        const int c = (q * kPlanThreads + tid) * 8;
+        *reinterpret_cast<u32x4*>(a.pool_k + dst + c) = kr[p][q];
+        *reinterpret_cast<u32x4*>(&tile[p][c]) = vr[p][q];
+      }
+    }
+    __syncthreads();
+    // V: [BS][d] -> [d][BS]; thread -> (d, 8-token group)
+    constexpr int kGroups = BS / 8;
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+      if (page[p] < 0) continue;
+      const long long dst = (((long long)r * (a.k + 1) + slot[p]) * a.Hkv + h) * kElems;
+#pragma unroll
+      for (int w = tid; w < kHeadDim * kGroups; w += kPlanThreads) {
+        const int d = w / kGroups;
+        const int t0 = (w % kGroups) * 8;
+        u32x4 o;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t lo = tile[p][(t0 + 2 * j) * kHeadDim + d];
+          const uint32_t hi = tile[p][(t0 + 2 * j + 1) * kHeadDim + d];
+          o[j] = lo | (hi << 16);
+        }
+        *reinterpret_cast<u32x4*>(a.pool_v + dst + (long long)d * BS + t0) = o;
+      }
+    }
+    __syncthreads();
+  }
+  __syncthreads();  // LDS plan arrays are reused by the next pair
   }
 }
 
 }  // namespace
 
-size_t stage_workspace_bytes(int R, int Hkv, int k) {
-  const size_t nrh = (size_t)R * Hkv;
-  return nrh * (size_t)k * sizeof(PlanEntry) + nrh * sizeof(int32_t);
+template <int BS>
+hipError_t launch_bs(const StageArgs& a, hipStream_t s) {
+  const int nrh = a.R * a.Hkv;
+  const int grid = nrh < kCopyWorkgroups ? nrh : kCopyWorkgroups;
+  const int pf = kCopyInflight / grid;  // entries per workgroup batch
+  if (pf >= 8)
+    hipLaunchKernelGGL((stage_kernel<BS, 8>), dim3(grid), dim3(kPlanThreads), 0, s, a);
+  else if (pf >= 4)
+    hipLaunchKernelGGL((stage_kernel<BS, 4>), dim3(grid), dim3(kPlanThreads), 0, s, a);
+  else if (pf >= 2)
+    hipLaunchKernelGGL((stage_kernel<BS, 2>), dim3(grid), dim3(kPlanThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL((stage_kernel<BS, 1>), dim3(grid), dim3(kPlanThreads), 0, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_stage(const StageArgs& a, hipStream_t s) {
-  const unsigned nrh = (unsigned)(a.R * a.Hkv);
-  if (!a.local_only) {
-    hipLaunchKernelGGL(stage_plan_kernel, dim3(nrh), dim3(kPlanThreads), 0, s, a);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  const dim3 grid(a.local_only ? 1u : (unsigned)(a.k + 1), nrh);
-  if (a.B == 16)
-    hipLaunchKernelGGL(stage_gather_kernel<16>, grid, dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL(stage_gather_kernel<32>, grid, dim3(256), 0, s, a);
-  return hipGetLastError();
+  return a.B == 16 ? launch_bs<16>(a, s) : launch_bs<32>(a, s);
 }
 
 }  // namespace oasis

@@ -2,7 +2,8 @@
 // blocks of 16 tokens, and the budget is the sparsification threshold).
 //
 // One 1024-thread workgroup per (request, KV head). Scores are mapped to
-// order-preserving uint32 keys (-0 folded into +0). A 4-pass, 8-bit radix
+// order-preserving uint32 keys (-0 folded into +0) and held in registers. A
+// 4-pass, 8-bit radix
 // select over an LDS histogram finds the exact key tau of the k-th largest
 // score and how many of the keys equal to tau are needed. Each thread owns a
 // contiguous range of block ids, so two block-wide exclusive scans give (1)
@@ -52,6 +53,9 @@ __device__ int block_exclusive_scan(int v, int* s_wave) {
   return res;
 }
 
+// Keys live in registers (KPT per thread, contiguous ids per thread); with
+// KPT == 0 they are re-read from global memory (very long contexts).
+template <int KPT>
 __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
   const int rh = blockIdx.x;
   const int r = rh / a.Hkv;
@@ -74,7 +78,16 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
   const float* s = a.scores + (long long)rh * a.NBmax;
   const int per = (n + kThreads - 1) / kThreads;
   const int lo = min(n, tid * per);
-  const int hi = min(n, lo + per);
+  const int cnt_local = min(n, lo + per) - lo;
+
+  constexpr int kRegs = KPT > 0 ? KPT : 1;
+  uint32_t keys[kRegs];
+  if (KPT > 0) {
+#pragma unroll
+    for (int j = 0; j < kRegs; ++j) keys[j] = j < cnt_local ? order_key(s[lo + j]) : 0u;
+  }
+  auto key_at = [&](int j) -> uint32_t { return KPT > 0 ? keys[j] : order_key(s[lo + j]); };
+  const int jmax = KPT > 0 ? kRegs : cnt_local;
 
   if (tid == 0) {
     s_digit = 0;
@@ -87,20 +100,22 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
     if (tid < 256) hist[tid] = 0u;
     __syncthreads();
     uint32_t cur = 0xFFFFFFFFu;
-    uint32_t cnt = 0u;
-    for (int i = lo; i < hi; ++i) {
-      const uint32_t key = order_key(s[i]);
+    uint32_t run = 0u;
+#pragma unroll
+    for (int j = 0; j < jmax; ++j) {
+      if (j >= cnt_local) break;
+      const uint32_t key = key_at(j);
       if ((key & mask) != prefix) continue;
       const uint32_t dg = (key >> shift) & 0xFFu;
       if (dg == cur) {
-        ++cnt;
+        ++run;
       } else {
-        if (cnt) atomicAdd(&hist[cur], cnt);
+        if (run) atomicAdd(&hist[cur], run);
         cur = dg;
-        cnt = 1u;
+        run = 1u;
       }
     }
-    if (cnt) atomicAdd(&hist[cur], cnt);
+    if (run) atomicAdd(&hist[cur], run);
     __syncthreads();
     if (tid < 64) {
       // lane L looks at bins 255-4L .. 252-4L (descending)
@@ -140,37 +155,28 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
   const uint32_t tau = prefix;
   const int need_eq = rem;  // how many tau-valued keys are taken, lowest ids first
 
-  int n_eq = 0;
-  for (int i = lo; i < hi; ++i) n_eq += order_key(s[i]) == tau;
-  const int eq_base = block_exclusive_scan(n_eq, s_wave);
-
-  int n_sel = 0;
-  {
-    int eq_rank = eq_base;
-    for (int i = lo; i < hi; ++i) {
-      const uint32_t key = order_key(s[i]);
-      if (key > tau) {
-        ++n_sel;
-      } else if (key == tau) {
-        n_sel += eq_rank < need_eq;
-        ++eq_rank;
-      }
-    }
+  int n_eq = 0, n_gt = 0;
+#pragma unroll
+  for (int j = 0; j < jmax; ++j) {
+    if (j >= cnt_local) break;
+    const uint32_t key = key_at(j);
+    n_eq += key == tau;
+    n_gt += key > tau;
   }
+  const int eq_base = block_exclusive_scan(n_eq, s_wave);
+  const int n_sel = n_gt + max(0, min(n_eq, need_eq - eq_base));
   int pos = block_exclusive_scan(n_sel, s_wave);
-  {
-    int eq_rank = eq_base;
-    for (int i = lo; i < hi; ++i) {
-      const uint32_t key = order_key(s[i]);
-      bool take = false;
-      if (key > tau) {
-        take = true;
-      } else if (key == tau) {
-        take = eq_rank < need_eq;
-        ++eq_rank;
-      }
-      if (take && pos < k) out[pos++] = i;
+  int eq_rank = eq_base;
+#pragma unroll
+  for (int j = 0; j < jmax; ++j) {
+    if (j >= cnt_local) break;
+    const uint32_t key = key_at(j);
+    bool take = key > tau;
+    if (key == tau) {
+      take = eq_rank < need_eq;
+      ++eq_rank;
     }
+    if (take && pos < k) out[pos++] = lo + j;
   }
   if (tid == 0) a.sel_count[rh] = k;
 }
@@ -178,7 +184,17 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
 }  // namespace
 
 hipError_t launch_topk(const TopkArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(topk_kernel, dim3((unsigned)(a.R * a.Hkv)), dim3(kThreads), 0, s, a);
+  // the candidate count of every request is at most NBmax - 1
+  const int per = (a.NBmax + kThreads - 1) / kThreads;
+  const dim3 grid((unsigned)(a.R * a.Hkv));
+  if (per <= 8)
+    hipLaunchKernelGGL(topk_kernel<8>, grid, dim3(kThreads), 0, s, a);
+  else if (per <= 16)
+    hipLaunchKernelGGL(topk_kernel<16>, grid, dim3(kThreads), 0, s, a);
+  else if (per <= 32)
+    hipLaunchKernelGGL(topk_kernel<32>, grid, dim3(kThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(topk_kernel<0>, grid, dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -39,7 +39,6 @@ class LayerState:
         self.moved = torch.zeros((R, Hkv), dtype=i32, device=dev)
         self.out = torch.empty((R, self.T, Hq, D), dtype=bf, device=dev)
         self.lse = torch.empty((R, self.T, Hq), dtype=torch.float32, device=dev)
-        self.ws_stage = torch.empty(max(1, L.oasis_stage_workspace_bytes(d, k)), dtype=torch.uint8, device=dev)
         self.ws_attn = torch.empty(max(1, L.oasis_attn_workspace_bytes(d, self.T, k)), dtype=torch.uint8,
                                    device=dev)
         self.ev_staged = None   # recorded after the last stage of this layer
@@ -95,7 +94,9 @@ class DecodePath:
         self.num_draft = int(num_draft if num_draft is not None else self.T - self.first_draft)
         self.host_k, self.host_v, self.block_table = host_k, host_v, block_table
         self.scale = scale if scale is not None else 1.0 / math.sqrt(d.head_dim)
-        self.side = torch.cuda.Stream()  # default priority
+        # background streams (default priority): top-K prediction, KV transfer
+        self.side = torch.cuda.Stream()
+        self.xfer = torch.cuda.Stream()
 
     def new_layer(self) -> LayerState:
         return LayerState(self.dims, self.T, self.k, self.block_table.device)
@@ -115,12 +116,12 @@ class DecodePath:
               copy_local: bool = True):
         L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, st.sel, st.sel_count,
                              self.k, st.slot_map, st.slot_stamp, step, self.k if fetch_cap is None else fetch_cap,
-                             copy_local, st.pool_k, st.pool_v, st.moved, st.ws_stage, stream)
+                             copy_local, st.pool_k, st.pool_v, st.moved, stream)
 
     def refresh_local(self, st: LayerState, ctx_len: torch.Tensor, stream=None):
         """Write the active local block into slot k (stands in for the model's KV write)."""
         L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, None, None, self.k,
-                             None, None, 0, self.k, True, st.pool_k, st.pool_v, None, None, stream)
+                             None, None, 0, self.k, True, st.pool_k, st.pool_v, None, stream)
 
     def attend(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, stream=None):
         L.oasis_sparse_decode_attn(self.dims, q, self.T, st.pool_k, st.pool_v, st.slot_map, self.k, ctx_len,
@@ -135,27 +136,31 @@ class DecodePath:
 
     def step_pipelined(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, step: int,
                        growing: bool = False, timer: KernelTimer | None = None, moved: torch.Tensor | None = None):
-        """One steady-state step (paper §4.2.2, one layer).
+        """One steady-state step of one layer (paper §4.2.2 pipeline).
 
         Foreground (current stream): wait for this layer's previous transfer,
         then attention of all T rows over the working set it produced.
-        Background (side stream): score + select from the draft rows of ``q``
-        concurrently with the attention, then, once the attention no longer
-        reads the pools, stage the new selection for the next step.
+        Prediction stream: score + select from the draft rows of ``q``,
+        concurrently with the attention. Transfer stream: once the selection
+        is ready and the attention no longer reads the pools, stage the new
+        selection for this layer's next step. Consecutive calls for different
+        layers therefore overlap one layer's transfer with the next layer's
+        attention and prediction.
         With ``growing`` (one token appended per step) the local block is
         rewritten on the foreground before the attention, since it changes
-        every step; otherwise the background stage refreshes it.
+        every step; otherwise the transfer refreshes it.
         ``timer`` records HIP events around each call on its own stream;
         ``moved`` (int32 [R][Hkv]) receives the entries this step copies.
         """
         tm = timer if timer is not None else _NO_TIMER
         fg = torch.cuda.current_stream()
-        bg = self.side
+        pred, xfer = self.side, self.xfer
         ev_q = torch.cuda.Event()
         ev_q.record(fg)  # q and ctx_len are ready on the foreground
-        bg.wait_event(ev_q)
+        pred.wait_event(ev_q)
         if st.ev_staged is not None:
             fg.wait_event(st.ev_staged)
+            pred.wait_event(st.ev_staged)  # the previous transfer of this layer read sel
         if growing:
             self.refresh_local(st, ctx_len, fg)
         e = tm.begin("attn", fg)
@@ -163,25 +168,30 @@ class DecodePath:
         tm.end("attn", fg, e)
         ev_attn = torch.cuda.Event()
         ev_attn.record(fg)
-        e = tm.begin("score", bg)
+        e = tm.begin("score", pred)
         L.oasis_score_blocks(self.dims, q, self.T, self.first_draft, self.num_draft, st.kmax, st.kmin, ctx_len,
-                             st.scores, bg)
-        tm.end("score", bg, e)
-        e = tm.begin("topk", bg)
-        L.oasis_select_topk(self.dims, st.scores, ctx_len, self.k, st.sel, st.sel_count, bg)
-        tm.end("topk", bg, e)
-        bg.wait_event(ev_attn)  # the gather overwrites slots the attention reads
-        e = tm.begin("stage", bg)
+                             st.scores, pred)
+        tm.end("score", pred, e)
+        e = tm.begin("topk", pred)
+        L.oasis_select_topk(self.dims, st.scores, ctx_len, self.k, st.sel, st.sel_count, pred)
+        tm.end("topk", pred, e)
+        ev_pred = torch.cuda.Event()
+        ev_pred.record(pred)
+        xfer.wait_event(ev_pred)
+        xfer.wait_event(ev_attn)  # the gather overwrites slots the attention reads
+        e = tm.begin("stage", xfer)
         L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, st.sel, st.sel_count,
                              self.k, st.slot_map, st.slot_stamp, step, self.k, not growing, st.pool_k, st.pool_v,
-                             st.moved if moved is None else moved, st.ws_stage, bg)
-        tm.end("stage", bg, e)
+                             st.moved if moved is None else moved, xfer)
+        tm.end("stage", xfer, e)
         ev_staged = torch.cuda.Event()
-        ev_staged.record(bg)
+        ev_staged.record(xfer)
         st.ev_staged, st.ev_attended = ev_staged, ev_attn
 
     def join(self):
-        torch.cuda.current_stream().wait_stream(self.side)
+        fg = torch.cuda.current_stream()
+        fg.wait_stream(self.side)
+        fg.wait_stream(self.xfer)
 
 
 class _NullTimer(KernelTimer):

@@ -32,8 +32,7 @@ def lib():
 def test_header_declares_the_path():
     names = declared()
     for fn in ("oasis_score_blocks", "oasis_select_topk", "oasis_stage_blocks", "oasis_sparse_decode_attn",
-               "oasis_build_summaries", "oasis_attn_workspace_bytes", "oasis_stage_workspace_bytes",
-               "oasis_last_error", "oasis_abi_version"):
+               "oasis_build_summaries", "oasis_attn_workspace_bytes", "oasis_last_error", "oasis_abi_version"):
         assert fn in names
 
 
@@ -73,7 +72,10 @@ def test_argument_checks_without_gpu(lib):
                                       None, 0, None) == 2
     # capped eviction is not implemented yet: explicit UNSUPPORTED
     assert L.oasis_stage_blocks(ctypes.byref(d), None, None, 10, None, None, None, None, 128, None, None, 0, 6, 1,
-                                None, None, None, None, 0, None) == 2
+                                None, None, None, None) == 2
+    # local-only form needs copy_local
+    assert L.oasis_stage_blocks(ctypes.byref(d), None, None, 10, None, None, None, None, 128, None, None, 0, 128, 0,
+                                None, None, None, None) == 1
     # zero requests: a no-op that succeeds without touching the device
     z = lib.dims(0, 32, 8, 128, 16, 512)
     assert L.oasis_score_blocks(ctypes.byref(z), None, 5, 1, 4, None, None, None, None, None) == 0
@@ -84,6 +86,4 @@ def test_workspace_sizes(lib):
     d = lib.dims(8, 32, 8, 128, 16, 8192)
     ws = lib.oasis_attn_workspace_bytes(d, 5, 128)
     assert ws > 0 and ws % 4 == 0
-    assert lib.oasis_stage_workspace_bytes(d, 128) == 8 * 8 * 128 * 8 + 8 * 8 * 4
-    assert lib.oasis_stage_workspace_bytes(d, 2048) == 0       # k above the plan kernel's limit
     assert lib.oasis_attn_workspace_bytes(lib.dims(1, 32, 8, 64, 16, 1), 5, 4) == 0

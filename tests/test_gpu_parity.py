@@ -113,6 +113,8 @@ SELECT_CASES = [
     (6, 2, 3, 2100, 32, [67200, 50000], 256, None),
     (7, 1, 1, 64, 16, [1024], 4096, None),                    # k far above the candidates
     (8, 2, 2, 5000, 16, [80000, 80000], 4000, 50),            # large k, ties
+    (9, 1, 2, 40000, 16, [640000], 128, None),                # keys re-read from memory (> 32768 candidates)
+    (10, 2, 2, 20000, 16, [320000, 200000], 300, 7),          # 16-32 keys per thread
 ]
 
 
@@ -369,6 +371,5 @@ def test_abi_errors_on_device():
     with pytest.raises(P.OasisError) as e:
         P.oasis_stage_blocks(d, host.pin_memory(), host.pin_memory(), torch.zeros((1, 16), dtype=torch.int32,
                              device="cuda"), ctx, smap, torch.zeros((1, 8), dtype=torch.int32, device="cuda"), k,
-                             smap, smap.clone(), 0, k - 1, True, pool, pool, None,
-                             torch.empty(1 << 16, dtype=torch.uint8, device="cuda"))
+                             smap, smap.clone(), 0, k - 1, True, pool, pool, None)
     assert e.value.status == 2  # capped eviction not implemented yet

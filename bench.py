@@ -292,7 +292,7 @@ def dense_attention(P, torch, w, hk_t, hv_t, ctx_d, d, c, iters=20):
     smap = torch.arange(ks, dtype=torch.int32, device="cuda").repeat(R * H).view(R, H, ks).contiguous()
     out = torch.empty((R, c.T, c.num_q_heads, D), dtype=torch.bfloat16, device="cuda")
     lse = torch.empty((R, c.T, c.num_q_heads), dtype=torch.float32, device="cuda")
-    ws = torch.empty(P.oasis_attn_workspace_bytes(d, c.T, ks), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(P.oasis_attn_workspace_bytes(d, c.T, ks), dtype=torch.uint8, device="cuda")
     q = torch.randn((R, c.T, c.num_q_heads, D), device="cuda").to(torch.bfloat16)
     for _ in range(3):
         P.oasis_sparse_decode_attn(d, q, c.T, pool_k, pool_v, smap, ks, ctx_d, None, out, lse, ws)

@@ -182,7 +182,8 @@ OASIS_API oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t
                                 int32_t copy_local, uint16_t* pool_k, uint16_t* pool_v, int32_t* moved,
                                 void* stream);
 
-/* Bytes of workspace oasis_sparse_decode_attn needs for these sizes (0 if invalid). */
+/* Bytes of workspace oasis_sparse_decode_attn needs for these sizes (0 if invalid).
+ * Calls that run at the same time need separate workspaces. */
 OASIS_API size_t oasis_attn_workspace_bytes(const oasis_dims* dims, int32_t num_q_tokens, int32_t k_slots);
 
 /*

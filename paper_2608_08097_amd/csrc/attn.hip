@@ -7,9 +7,12 @@
 // (request, KV head) are cut into units of 32 tokens (two slots at B = 16,
 // one at B = 32); a workgroup of 4 waves handles a contiguous range of units
 // (a split) and every wave a strided subset of them, with its own online
-// softmax. The waves are merged through LDS, each split writes one partial
-// (unnormalised output, running max, running sum) per row, and a second kernel
-// merges the splits and writes bf16 outputs and the log-sum-exp.
+// softmax. The waves are merged through LDS; with one split the workgroup
+// writes the bf16 outputs and the log-sum-exp itself, otherwise each split
+// writes one partial (unnormalised output, running max, running sum) per row
+// and a second kernel merges the splits. (A last-arriving-workgroup merge in
+// the same kernel measured slower on MI355X: its agent-scope release/acquire
+// costs more than the second launch.)
 //
 // One 32-token unit for one 16-row tile:
 //   S^T (tokens x rows) = K (tokens x d) . Q^T (d x rows): 2 token tiles x
@@ -59,72 +62,53 @@ struct UnitRegs {
   int n0, n1;
 };
 
+// Unit u (wave-uniform) covers slots s0 = 2u, s1 = 2u + 1 at B = 16 or slot u
+// at B = 32. Every load is unconditional: a slot index past the pool is
+// clamped onto the local slot (always inside the pool) and only the token
+// counts n0 / n1 decide which tokens count. Free slots may hold anything,
+// even NaN; their K only yields masked scores and their V is cleared below.
+//
+// u < 0 is a placeholder unit: the loads are issued anyway (on the local slot,
+// which is cache-resident after its first read) and count nothing. Issuing
+// the same number of loads on every path keeps the compiler's wait counts
+// exact, so waiting for the current unit never drains the prefetched one.
 template <int BS>
 __device__ __forceinline__ void load_unit(UnitRegs& ur, int u, int ks, int local_len, const int32_t* smap,
                                           const uint16_t* pk, const uint16_t* pv, long long slot_elems, int g,
                                           int i) {
-  // u is wave-uniform. Every slot <= ks lies inside the pool, so the K/V loads
-  // are issued without waiting for the slot map; its entries only decide
-  // afterwards which tokens count (free slots may hold anything, even NaN).
-  int s0, s1;
-  if (BS == 16) {
-    s0 = 2 * u;
-    s1 = 2 * u + 1;
-  } else {
-    s0 = u;
-    s1 = ks + 1;
-  }
-  const bool in0 = s0 <= ks, in1 = s1 <= ks;
+  const bool real = u >= 0;
+  const int s0 = real ? (BS == 16 ? 2 * u : u) : ks;
+  const int s1raw = real ? (BS == 16 ? 2 * u + 1 : ks + 1) : ks + 1;
+  const int s1 = s1raw <= ks ? s1raw : ks;
+  const uint16_t* k0 = pk + (long long)s0 * slot_elems;
+  const uint16_t* k1 = pk + (long long)s1 * slot_elems;
+  const uint16_t* v0 = pv + (long long)s0 * slot_elems;
+  const uint16_t* v1 = pv + (long long)s1 * slot_elems;
   // K: lane (g, i), token tile tau -> unit token 8*(i/4) + 4*tau + i%4
 #pragma unroll
   for (int tau = 0; tau < 2; ++tau) {
     const int tok = 8 * (i >> 2) + 4 * tau + (i & 3);
-    int slot, row;
-    bool in;
-    if (BS == 16) {
-      slot = tok < 16 ? s0 : s1;
-      row = tok & 15;
-      in = tok < 16 ? in0 : in1;
-    } else {
-      slot = s0;
-      row = tok;
-      in = in0;
-    }
-    const uint16_t* src = pk + (long long)(in ? slot : 0) * slot_elems + row * kHeadDim + g * 8;
+    const uint16_t* src = BS == 16 ? ((tok < 16 ? k0 : k1) + (tok & 15) * kHeadDim + g * 8)
+                                   : (k0 + tok * kHeadDim + g * 8);
 #pragma unroll
-    for (int st = 0; st < 4; ++st) ur.k[tau][st] = in ? ldg16(src + st * 32) : u32x4{0, 0, 0, 0};
+    for (int st = 0; st < 4; ++st) ur.k[tau][st] = ldg16(src + st * 32);
   }
   // V^T: lane (g, i), d-tile dt -> V[tokens 8g .. 8g+7][d = dt*16 + i]
-  int vslot, t0;
-  bool vin;
-  if (BS == 16) {
-    vslot = g < 2 ? s0 : s1;
-    t0 = (g & 1) * 8;
-    vin = g < 2 ? in0 : in1;
-  } else {
-    vslot = s0;
-    t0 = 8 * g;
-    vin = in0;
-  }
-  const uint16_t* src = pv + (long long)(vin ? vslot : 0) * slot_elems + t0;
+  const uint16_t* vsrc = BS == 16 ? ((g < 2 ? v0 : v1) + (g & 1) * 8) : (v0 + 8 * g);
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) ur.v[dt] = vin ? ldg16(src + (long long)(dt * 16 + i) * BS) : u32x4{0, 0, 0, 0};
+  for (int dt = 0; dt < 8; ++dt) ur.v[dt] = ldg16(vsrc + (long long)(dt * 16 + i) * BS);
   // token counts of the two slots (0 = not attended)
-  const int n0 = s0 < ks ? (smap[s0] >= 0 ? BS : 0) : (s0 == ks ? local_len : 0);
-  int n1 = 0;
-  if (BS == 16) n1 = s1 < ks ? (smap[s1] >= 0 ? BS : 0) : (s1 == ks ? local_len : 0);
-  ur.n0 = n0;
-  ur.n1 = n1;
+  ur.n0 = !real ? 0 : (s0 < ks ? (smap[s0] >= 0 ? BS : 0) : (s0 == ks ? local_len : 0));
+  ur.n1 = (BS == 16 && real) ? (s1raw < ks ? (smap[s1raw] >= 0 ? BS : 0) : (s1raw == ks ? local_len : 0)) : 0;
 }
 
 // Zero the V values of tokens that are not attended (their probability is 0,
-// but 0 * NaN would poison the accumulator).
+// but 0 * NaN would poison the accumulator). Branch-free on purpose.
 template <int BS>
 __device__ __forceinline__ void mask_unit_v(UnitRegs& ur, int g) {
   const int cnt = BS == 16 ? (g < 2 ? ur.n0 : ur.n1) : ur.n0;
   const int t0 = BS == 16 ? (g & 1) * 8 : 8 * g;
   const int keep = cnt - t0;
-  if (keep >= 8) return;
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
@@ -205,6 +189,19 @@ __device__ __forceinline__ void process_unit(const UnitRegs& cur, const bf16x8 (
   }
 }
 
+// Normalised bf16 output of 4 dimensions of one row, and its log-sum-exp.
+__device__ __forceinline__ void write_output(const AttnArgs& a, int r, int h, int row, int c4, f32x4 o, float M,
+                                             float L) {
+  const int t = row / a.G;
+  const int qh = h * a.G + (row - t * a.G);
+  const long long orow = ((long long)r * a.T + t) * a.Hq + qh;
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  const uint32_t w0 = f32_to_bf16_bits(o[0] * inv) | (f32_to_bf16_bits(o[1] * inv) << 16);
+  const uint32_t w1 = f32_to_bf16_bits(o[2] * inv) | (f32_to_bf16_bits(o[3] * inv) << 16);
+  *reinterpret_cast<uint2*>(a.out + orow * kHeadDim + c4 * 4) = make_uint2(w0, w1);
+  if (c4 == 0 && a.lse) a.lse[orow] = L > 0.f ? (M + __log2f(L)) * 0.69314718055994531f : -INFINITY;
+}
+
 template <int NT, int BS>
 __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
@@ -261,13 +258,19 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   constexpr bool kPrefetch = NT <= 2;
   int u = u_begin + wave;
   if (kPrefetch) {
-    UnitRegs cur, nxt;
-    if (u < u_end) load_unit<BS>(cur, u, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
-    for (; u < u_end; u += kW) {
-      if (u + kW < u_end) load_unit<BS>(nxt, u + kW, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
-      mask_unit_v<BS>(cur, g);
-      process_unit<NT, BS>(cur, qb, m_run, l_run, acc, g, a.scale_log2);
-      cur = nxt;
+    // two register buffers used alternately (no copies between them)
+    UnitRegs ua, ub;
+    load_unit<BS>(ua, u < u_end ? u : -1, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
+    while (u < u_end) {
+      load_unit<BS>(ub, u + kW < u_end ? u + kW : -1, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
+      mask_unit_v<BS>(ua, g);
+      process_unit<NT, BS>(ua, qb, m_run, l_run, acc, g, a.scale_log2);
+      u += kW;
+      if (u >= u_end) break;
+      load_unit<BS>(ua, u + kW < u_end ? u + kW : -1, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
+      mask_unit_v<BS>(ub, g);
+      process_unit<NT, BS>(ub, qb, m_run, l_run, acc, g, a.scale_log2);
+      u += kW;
     }
   } else {
     for (; u < u_end; u += kW) {
@@ -285,11 +288,15 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   }
 
   // ---- merge the waves of this workgroup through LDS -----------------------
+  // Row maxima first; every wave rescales its accumulators to them and writes
+  // them to a slice (kSlices slices; with fewer slices than waves the other
+  // waves add into them in a second round); then every thread sums the slices
+  // of some (row, dimension) entries in a fixed order.
   constexpr int kRows = NT * 16;
   constexpr int kPad = kHeadDim + 4;
+  constexpr int kSlices = NT <= 4 ? kW : 2;  // LDS: kSlices * kRows * kPad floats <= 160 KiB
   __shared__ float s_m[kW][kRows], s_l[kW][kRows];
-  __shared__ float s_M[kRows], s_L[kRows];
-  __shared__ float s_o[kRows][kPad];
+  __shared__ float s_o[kSlices][kRows][kPad];
   if (g == 0) {
 #pragma unroll
     for (int v = 0; v < NT; ++v) {
@@ -307,24 +314,18 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
     const float f = M == -INFINITY ? 0.f : fast_exp2(m_run[v] - M);
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) acc[v][dt] *= f;
-    if (wave == 0 && g == 0) {
-      float L = 0.f;
-#pragma unroll
-      for (int w = 0; w < kW; ++w) L += M == -INFINITY ? 0.f : s_l[w][row] * fast_exp2(s_m[w][row] - M);
-      s_M[row] = M;
-      s_L[row] = L;
-    }
   }
 #pragma unroll
-  for (int w = 0; w < kW; ++w) {
-    if (wave == w) {
+  for (int round = 0; round < kW / kSlices; ++round) {
+    if (wave / kSlices == round) {
+      const int sl = wave % kSlices;
 #pragma unroll
       for (int v = 0; v < NT; ++v)
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
-          float* dst = &s_o[v * 16 + i][dt * 16 + 4 * g];
+          float* dst = &s_o[sl][v * 16 + i][dt * 16 + 4 * g];
           f32x4 val = acc[v][dt];
-          if (w > 0) {
+          if (round > 0) {
             val[0] += dst[0];
             val[1] += dst[1];
             val[2] += dst[2];
@@ -339,22 +340,44 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
     __syncthreads();
   }
 
-  // ---- write this split's partial ------------------------------------------
-  const long long pbase = ((long long)rh * a.nsplit + split) * a.rows;
+  const int nsplit = a.nsplit;
+  const long long pbase = ((long long)rh * nsplit + split) * a.rows;
+  // (row, 4-dimension group) entries of this split: max over waves, rescale, sum
   for (int idx = threadIdx.x; idx < a.rows * (kHeadDim / 4); idx += kW * 64) {
     const int row = idx / (kHeadDim / 4);
     const int c4 = idx - row * (kHeadDim / 4);
-    const float* src = &s_o[row][c4 * 4];
-    *reinterpret_cast<f32x4*>(a.part_o + (pbase + row) * kHeadDim + c4 * 4) = f32x4{src[0], src[1], src[2], src[3]};
-  }
-  for (int row = threadIdx.x; row < a.rows; row += kW * 64) {
-    a.part_ml[(pbase + row) * 2 + 0] = s_M[row];
-    a.part_ml[(pbase + row) * 2 + 1] = s_L[row];
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kW; ++w) M = fmaxf(M, s_m[w][row]);
+    f32x4 o = {0.f, 0.f, 0.f, 0.f};
+    float L = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+      for (int w = 0; w < kW; ++w) L += s_m[w][row] == -INFINITY ? 0.f : s_l[w][row] * fast_exp2(s_m[w][row] - M);
+#pragma unroll
+      for (int sl = 0; sl < kSlices; ++sl) {
+        const float* src = &s_o[sl][row][c4 * 4];
+        o[0] += src[0];
+        o[1] += src[1];
+        o[2] += src[2];
+        o[3] += src[3];
+      }
+    }
+    if (nsplit == 1) {  // the only split: finish here
+      write_output(a, r, h, row, c4, o, M, L);
+    } else {
+      *reinterpret_cast<f32x4*>(a.part_o + (pbase + row) * kHeadDim + c4 * 4) = o;
+      if (c4 == 0) {
+        a.part_ml[(pbase + row) * 2 + 0] = M;
+        a.part_ml[(pbase + row) * 2 + 1] = L;
+      }
+    }
   }
 }
 
-// One workgroup per (row, request x KV head); one thread per dimension. All
-// partial loads of a thread are issued before any is used (nsplit <= kMaxSplits).
+// Merge of the splits: one workgroup per (row, request x KV head), one thread
+// per dimension; all partial loads of a thread are issued before any is used
+// (nsplit <= kMaxSplits).
 __global__ __launch_bounds__(kHeadDim) void attn_merge_kernel(AttnArgs a) {
   const int row = blockIdx.x;
   const int rh = blockIdx.y;
@@ -397,7 +420,7 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
   const int nrh8 = (nrh + 7) / 8 * 8;
   hipLaunchKernelGGL((attn_split_kernel<NT, BS>), dim3((unsigned)(nrh8 * a.nsplit)), dim3(kW * 64), 0, s, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || a.nsplit == 1) return e;
   hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)a.rows, (unsigned)nrh), dim3(kHeadDim), 0, s, a);
   return hipGetLastError();
 }

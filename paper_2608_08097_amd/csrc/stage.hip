@@ -35,8 +35,8 @@ namespace {
 constexpr int kPlanThreads = 256;
 constexpr int kMaxK = 1024;
 constexpr int kPer = kMaxK / kPlanThreads;  // items per thread in the scans
-constexpr int kCopyWorkgroups = 16;
-constexpr int kCopyInflight = 16;  // block-head entries (K and V) in flight over the whole grid
+constexpr int kCopyWorkgroups = 32;
+constexpr int kCopyInflight = 32;  // block-head entries (K and V) in flight over the whole grid
 
 __device__ int wg_exclusive_scan(int v, int* s_wave) {
   const int lane = threadIdx.x & 63;

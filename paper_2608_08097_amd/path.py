@@ -39,7 +39,7 @@ class LayerState:
         self.moved = torch.zeros((R, Hkv), dtype=i32, device=dev)
         self.out = torch.empty((R, self.T, Hq, D), dtype=bf, device=dev)
         self.lse = torch.empty((R, self.T, Hq), dtype=torch.float32, device=dev)
-        self.ws_attn = torch.empty(max(1, L.oasis_attn_workspace_bytes(d, self.T, k)), dtype=torch.uint8,
+        self.ws_attn = torch.zeros(max(1, L.oasis_attn_workspace_bytes(d, self.T, k)), dtype=torch.uint8,
                                    device=dev)
         self.ev_staged = None   # recorded after the last stage of this layer
         self.ev_attended = None  # recorded after the last attention of this layer

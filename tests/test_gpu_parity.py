@@ -242,7 +242,7 @@ def test_attn(seed, R, Hq, Hkv, T, B, ks, lens, free):
     d = P.dims(R, Hq, Hkv, d_head, B, max(1, (int(ctx.max()) + B - 1) // B))
     out = torch.zeros((R, T, Hq, d_head), dtype=torch.bfloat16, device="cuda")
     lse = torch.zeros((R, T, Hq), dtype=torch.float32, device="cuda")
-    ws = torch.empty(P.oasis_attn_workspace_bytes(d, T, ks), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(P.oasis_attn_workspace_bytes(d, T, ks), dtype=torch.uint8, device="cuda")
     P.oasis_sparse_decode_attn(d, dev_bf16(q), T, dev_bf16(pk), dev_bf16(pool_v_from_htd(pv)),
                                dev_i32(smap) if ks else None, ks, dev_i32(ctx), None, out, lse, ws)
     torch.cuda.synchronize()

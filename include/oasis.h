@@ -66,7 +66,7 @@
 extern "C" {
 #endif
 
-#define OASIS_ABI_VERSION 1
+#define OASIS_ABI_VERSION 2
 
 /* Only the entry points below are exported from liboasis.so. */
 #if defined(__GNUC__) || defined(__clang__)
@@ -152,9 +152,15 @@ OASIS_API oasis_status oasis_select_topk(const oasis_dims* dims, const float* sc
  * over PCIe and writes them into the resident GPU pages).
  *
  * For every (r, h), with S = sel[r][h][0..sel_count) (ascending, as produced by
- * oasis_select_topk): misses = S minus the resident blocks (ascending); victims =
+ * oasis_select_topk): misses = S minus the resident blocks; admitted = all
+ * misses, or, when there are more than fetch_cap, the fetch_cap misses with the
+ * highest scores[r][h][block] (equal scores: lower block id; §4.2.3 caps the
+ * pairs per KV head and step, §5.5.1 sets the cap as a fraction of K); victims =
  * free slots (ascending), then resident non-selected slots by (slot_stamp, slot);
- * the i-th miss goes to the i-th victim: its K entry (B x d) is copied from
+ * the i-th admitted miss in ascending block id goes to the i-th victim; slots
+ * that receive nothing keep their block and stamp (a non-admitted miss is absent
+ * for this step, and stale residents keep being attended). Each admitted block's
+ * K entry (B x d) is copied from
  * host_k page host_block_table[r][block] head h into pool_k[r][slot][h], its V
  * entry into pool_v[r][slot][h] (transposed to d x B). slot_map is updated and
  * every slot that holds a selected block afterwards gets slot_stamp = step.
@@ -167,8 +173,11 @@ OASIS_API oasis_status oasis_select_topk(const oasis_dims* dims, const float* sc
  * only slot k is refreshed; slot_map, slot_stamp and moved may then be NULL. This stands in for the model writing the newest token's K/V
  * into the resident local block before attention.
  *
- * fetch_cap: most misses admitted per (r, h) per call; fetch_cap >= k means
- * uncapped. A cap below k is OASIS_ERR_UNSUPPORTED in this version.
+ * fetch_cap: most misses admitted per (r, h) per call, >= 1 (a fetch ratio rho
+ * gives max(1, floor(rho * k))); fetch_cap >= k means uncapped. scores: the
+ * [R][Hkv][max_blocks] fp32 output of oasis_score_blocks for this selection,
+ * read only when fetch_cap < k (may be NULL otherwise); any value ranks
+ * (order-preserving integer keys), so exactly min(fetch_cap, misses) are admitted.
  * host_k/host_v: pinned host memory (hipHostMalloc) or device memory; the
  * library resolves the device-visible address. Everything else: device.
  * sel must be strictly ascending within [0, sel_count); 1 <= k <= 1024.
@@ -177,7 +186,7 @@ OASIS_API oasis_status oasis_select_topk(const oasis_dims* dims, const float* sc
  */
 OASIS_API oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, const uint16_t* host_v,
                                 int64_t num_pages, const int32_t* host_block_table, const int32_t* ctx_len,
-                                const int32_t* sel, const int32_t* sel_count, int32_t k,
+                                const int32_t* sel, const int32_t* sel_count, const float* scores, int32_t k,
                                 int32_t* slot_map, int32_t* slot_stamp, int32_t step, int32_t fetch_cap,
                                 int32_t copy_local, uint16_t* pool_k, uint16_t* pool_v, int32_t* moved,
                                 void* stream);

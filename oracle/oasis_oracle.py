@@ -178,7 +178,8 @@ def select_topk(scores, ctx_len, k: int, block_size: int):
 # ---------------------------------------------------------------------------
 
 def stage_blocks(host_k, host_v, block_table, sel, sel_count, slot_map, slot_stamp,
-                 step: int, pool_k, pool_v, ctx_len, block_size: int, copy_local: bool = True):
+                 step: int, pool_k, pool_v, ctx_len, block_size: int, copy_local: bool = True,
+                 scores=None, fetch_cap: int | None = None):
     """Bring the selected blocks into the HBM working set; updates in place.
 
     Paper §4.2.3 (KV selection): the predicted set is intersected with the
@@ -191,12 +192,19 @@ def stage_blocks(host_k, host_v, block_table, sel, sel_count, slot_map, slot_sta
     map); §5.1: the transfer copies block-head entries (K and V of B tokens of
     one head) from the host pages into the resident GPU pages.
 
-    Readings (R14): no fetch cap (every miss is admitted); free slots (-1) are
-    used first in ascending slot order, then non-selected residents by
-    (last-selected step, slot); misses are paired in ascending block id; every
-    slot that holds a selected block afterwards gets ``step`` as its stamp.
-    ``copy_local`` also refreshes slot K of every head with the local block
-    (reading R4: the local block is always attended).
+    Readings (R14): free slots (-1) are used first in ascending slot order,
+    then non-selected residents by (last-selected step, slot); admitted misses
+    are paired with the targets in ascending block id; every slot that holds a
+    selected block afterwards gets ``step`` as its stamp. ``copy_local`` also
+    refreshes slot K of every head with the local block (reading R4: the local
+    block is always attended).
+
+    Fetch cap (§4.2.3, §5.5.1): each KV head admits at most ``fetch_cap``
+    pairs per step and leaves every other slot as it is, so a selected block
+    that is not admitted is simply absent this step while the stale residents
+    that were not evicted keep being attended. Reading R15: the admitted misses
+    are the ``fetch_cap`` ones with the highest score in ``scores`` [R][Hkv][NB]
+    (ties: lowest block id). ``fetch_cap=None`` (or >= K) admits every miss.
 
     Returns the number of block-head entries moved per (request, KV head),
     excluding the local block.
@@ -217,6 +225,10 @@ def stage_blocks(host_k, host_v, block_table, sel, sel_count, slot_map, slot_sta
                            if slot_map[r, h, s] >= 0 and int(slot_map[r, h, s]) not in chosen_set)
             victims = free + [s for _, s in stale]
             assert len(victims) >= len(misses)
+            assert fetch_cap is None or fetch_cap >= 1
+            if fetch_cap is not None and len(misses) > fetch_cap:
+                by_score = sorted(misses, key=lambda b: (-float(scores[r, h, b]), b))
+                misses = sorted(by_score[:fetch_cap])
             for b, s in zip(misses, victims):
                 slot_map[r, h, s] = b
                 page = int(block_table[r][b])

@@ -75,7 +75,7 @@ def lib() -> ctypes.CDLL:
         L.oasis_select_topk.restype = _I32
         L.oasis_select_topk.argtypes = [_DIMS, _P, _P, _I32, _P, _P, _P]
         L.oasis_stage_blocks.restype = _I32
-        L.oasis_stage_blocks.argtypes = [_DIMS, _P, _P, _I64, _P, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
+        L.oasis_stage_blocks.argtypes = [_DIMS, _P, _P, _I64, _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
                                          _P, _P, _P, _P]
         L.oasis_attn_workspace_bytes.restype = _SZ
         L.oasis_attn_workspace_bytes.argtypes = [_DIMS, _I32, _I32]
@@ -180,7 +180,7 @@ def oasis_select_topk(d: OasisDims, scores, ctx_len, k: int, sel, sel_count, str
         _dev(sel, "sel", _I32T), _dev(sel_count, "sel_count", _I32T), _stream(stream)))
 
 
-def oasis_stage_blocks(d: OasisDims, host_k, host_v, host_block_table, ctx_len, sel, sel_count, k: int,
+def oasis_stage_blocks(d: OasisDims, host_k, host_v, host_block_table, ctx_len, sel, sel_count, scores, k: int,
                        slot_map, slot_stamp, step: int, fetch_cap: int, copy_local: bool, pool_k, pool_v,
                        moved, stream=None) -> None:
     if host_k.shape != host_v.shape:
@@ -192,13 +192,15 @@ def oasis_stage_blocks(d: OasisDims, host_k, host_v, host_block_table, ctx_len, 
     for t, n in ((sel, "sel"), (slot_map, "slot_map"), (slot_stamp, "slot_stamp")):
         _need(t, R * H * k, n)
     _need(sel_count, R * H, "sel_count")
+    _need(scores, R * H * d.max_blocks, "scores")
     _need(moved, R * H, "moved")
     _need(pool_k, R * (k + 1) * H * B * D, "pool_k")
     _need(pool_v, R * (k + 1) * H * B * D, "pool_v")
     _check("oasis_stage_blocks", lib().oasis_stage_blocks(
         ctypes.byref(d), _host_or_dev(host_k, "host_k", _BF16), _host_or_dev(host_v, "host_v", _BF16),
         int(host_k.shape[0]), _dev(host_block_table, "host_block_table", _I32T), _dev(ctx_len, "ctx_len", _I32T),
-        _dev(sel, "sel", _I32T, nullable=True), _dev(sel_count, "sel_count", _I32T, nullable=True), int(k),
+        _dev(sel, "sel", _I32T, nullable=True), _dev(sel_count, "sel_count", _I32T, nullable=True),
+        _dev(scores, "scores", (torch.float32,), nullable=True), int(k),
         _dev(slot_map, "slot_map", _I32T, nullable=True), _dev(slot_stamp, "slot_stamp", _I32T, nullable=True),
         int(step), int(fetch_cap), 1 if copy_local else 0, _dev(pool_k, "pool_k", _BF16),
         _dev(pool_v, "pool_v", _BF16), _dev(moved, "moved", _I32T, nullable=True), _stream(stream)))

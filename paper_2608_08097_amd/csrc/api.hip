@@ -143,16 +143,15 @@ oasis_status oasis_select_topk(const oasis_dims* dims, const float* scores, cons
 
 oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, const uint16_t* host_v,
                                 int64_t num_pages, const int32_t* host_block_table, const int32_t* ctx_len,
-                                const int32_t* sel, const int32_t* sel_count, int32_t k, int32_t* slot_map,
+                                const int32_t* sel, const int32_t* sel_count, const float* scores, int32_t k,
+                                int32_t* slot_map,
                                 int32_t* slot_stamp, int32_t step, int32_t fetch_cap, int32_t copy_local,
                                 uint16_t* pool_k, uint16_t* pool_v, int32_t* moved, void* stream) {
   static const char* fn = "oasis_stage_blocks";
   oasis_status st = check_dims(dims, fn);
   if (st != OASIS_OK) return st;
   if (k < 1 || k > 1024) return fail(OASIS_ERR_INVALID_ARG, "%s: k = %d outside [1, 1024]", fn, k);
-  if (fetch_cap < k)
-    return fail(OASIS_ERR_UNSUPPORTED, "%s: fetch_cap %d < k %d (capped eviction is not implemented)", fn,
-                fetch_cap, k);
+  if (fetch_cap < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: fetch_cap = %d < 1", fn, fetch_cap);
   if (copy_local != 0 && copy_local != 1) return fail(OASIS_ERR_INVALID_ARG, "%s: copy_local must be 0 or 1", fn);
   if (num_pages < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: num_pages < 1", fn);
   if ((sel == nullptr) != (sel_count == nullptr))
@@ -170,6 +169,7 @@ oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, 
   if (!local_only) {
     REQUIRE_PTR(slot_map, fn);
     REQUIRE_PTR(slot_stamp, fn);
+    if (fetch_cap < k) REQUIRE_PTR(scores, fn);
   }
   const void *hk = nullptr, *hv = nullptr;
   if ((st = device_view(host_k, &hk, "host_k", fn)) != OASIS_OK) return st;
@@ -182,6 +182,7 @@ oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, 
   a.ctx_len = ctx_len;
   a.sel = sel;
   a.sel_count = sel_count;
+  a.scores = scores;
   a.slot_map = slot_map;
   a.slot_stamp = slot_stamp;
   a.pool_k = pool_k;
@@ -195,6 +196,7 @@ oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, 
   a.k = k;
   a.step = step;
   a.copy_local = copy_local;
+  a.fetch_cap = fetch_cap < k ? fetch_cap : k;
   return hip_status(oasis::launch_stage(a, static_cast<hipStream_t>(stream)), fn);
 }
 

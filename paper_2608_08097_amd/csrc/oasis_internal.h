@@ -84,12 +84,14 @@ struct StageArgs {
   const int32_t* ctx_len;
   const int32_t* sel;
   const int32_t* sel_count;
+  const float* scores;      // [R][Hkv][NBmax], read only under a binding cap
   int32_t* slot_map;
   int32_t* slot_stamp;
   uint16_t* pool_k;
   uint16_t* pool_v;
   int32_t* moved;
   int R, Hkv, B, NBmax, k, step, copy_local;
+  int fetch_cap;            // admitted misses per (request, KV head), >= k: all
   int local_only;           // no selection: refresh the local block only
 };
 hipError_t launch_stage(const StageArgs& a, hipStream_t s);

@@ -3,7 +3,9 @@
 // Paper §4.2.3: the predicted set is intersected with the resident set (hits
 // stay, no bytes move), non-selected residents are ranked by the step at which
 // they were last selected and evicted least-recently-selected first, and each
-// admitted miss is paired with one eviction target. §4.3: a per-KV-head map
+// admitted miss is paired with one eviction target; at most fetch_cap pairs are
+// admitted per KV head and step (§5.5.1: a fetch ratio of K), the highest-
+// scoring misses first, and all other slots stay as they are. §4.3: a per-KV-head map
 // records which logical block each GPU slot holds. §5.1: a gather kernel reads
 // the selected block-head entries from pinned host memory over PCIe and
 // writes them into the resident GPU pages.
@@ -38,6 +40,13 @@ constexpr int kPer = kMaxK / kPlanThreads;  // items per thread in the scans
 constexpr int kCopyWorkgroups = 32;
 constexpr int kCopyInflight = 32;  // block-head entries (K and V) in flight over the whole grid
 
+// Monotone map of a float onto uint32 (larger float, larger key; -0 and +0 equal).
+__device__ inline unsigned order_key(float f) {
+  unsigned u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
 __device__ int wg_exclusive_scan(int v, int* s_wave) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -64,6 +73,7 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
   const int tid = threadIdx.x;
   const int k = a.k;
   __shared__ int s_sel[kMaxK], s_map[kMaxK], s_stamp[kMaxK], s_hit[kMaxK], s_keep[kMaxK], s_vict[kMaxK];
+  __shared__ unsigned s_key[kMaxK];
 
   const long long base = (long long)rh * k;
   int m = a.sel_count[rh];
@@ -105,10 +115,48 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
     if (i < m && !s_hit[i]) ++n_miss_local;
     if (i < k && s_map[i] < 0) ++n_free_local;
   }
-  const int miss_base = wg_exclusive_scan(n_miss_local, s_wave);
+  wg_exclusive_scan(n_miss_local, s_wave);
   const int n_miss = s_wave[4];
   const int free_base = wg_exclusive_scan(n_free_local, s_wave);
   const int n_free = s_wave[4];
+
+  // admission: every miss, or under a binding cap the fetch_cap misses with the
+  // highest score (ties: lowest block id, i.e. lowest selection index). Keys are
+  // order-preserving integers, so the ranks are distinct even for NaN scores and
+  // exactly fetch_cap misses are admitted.
+  const bool capped = a.fetch_cap < n_miss;
+  if (capped) {
+    for (int i = tid; i < m; i += kPlanThreads) {
+      const int b = s_sel[i];
+      const float sc = (b >= 0 && b < a.NBmax) ? a.scores[(long long)rh * a.NBmax + b] : -__builtin_inff();
+      s_key[i] = s_hit[i] ? 0u : order_key(sc);
+    }
+    __syncthreads();
+  }
+  unsigned adm_bits = 0;
+  int n_adm_local = 0;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int i = i0 + j;
+    if (i >= m || s_hit[i]) continue;
+    bool adm = true;
+    if (capped) {
+      const unsigned key = s_key[i];
+      int rank = 0;
+      for (int t = 0; t < m; ++t) {
+        if (s_hit[t]) continue;
+        const unsigned kt = s_key[t];
+        rank += (kt > key) || (kt == key && t < i);
+      }
+      adm = rank < a.fetch_cap;
+    }
+    if (adm) {
+      adm_bits |= 1u << j;
+      ++n_adm_local;
+    }
+  }
+  const int adm_base = wg_exclusive_scan(n_adm_local, s_wave);
+  const int n_adm = s_wave[4];
 
   // victim order: free slots ascending, then stale residents by (stamp, slot)
   {
@@ -132,14 +180,14 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
   }
   __syncthreads();
 
-  // pair the i-th miss with the i-th victim
+  // pair the i-th admitted miss (ascending block id) with the i-th victim
   int moved_local = 0;
   {
-    int mr = miss_base;
+    int mr = adm_base;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int i = i0 + j;
-      if (i >= m || s_hit[i]) continue;
+      if (!(adm_bits >> j & 1u)) continue;
       // a slot map holding one block twice can leave fewer victims than misses
       const int v = mr < k ? s_vict[mr] : -1;
       const int blk = s_sel[i];
@@ -164,7 +212,7 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
     if (s_keep[s]) a.slot_stamp[base + s] = a.step;
   }
   if (tid == 0 && a.moved) a.moved[rh] = moved;
-  return n_miss;
+  return n_adm;
 }
 
 template <int BS, int PF>

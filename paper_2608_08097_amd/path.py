@@ -88,8 +88,10 @@ class DecodePath:
 
     def __init__(self, d: L.OasisDims, num_q_tokens: int, k: int, host_k: torch.Tensor, host_v: torch.Tensor,
                  block_table: torch.Tensor, first_draft: int = 1, num_draft: int | None = None,
-                 scale: float | None = None):
+                 scale: float | None = None, fetch_cap: int | None = None):
         self.dims, self.T, self.k = d, int(num_q_tokens), int(k)
+        # admitted misses per (request, KV head) and step; k admits every miss
+        self.fetch_cap = self.k if fetch_cap is None else int(fetch_cap)
         self.first_draft = int(first_draft)
         self.num_draft = int(num_draft if num_draft is not None else self.T - self.first_draft)
         self.host_k, self.host_v, self.block_table = host_k, host_v, block_table
@@ -115,13 +117,14 @@ class DecodePath:
     def stage(self, st: LayerState, ctx_len: torch.Tensor, step: int, stream=None, fetch_cap: int | None = None,
               copy_local: bool = True):
         L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, st.sel, st.sel_count,
-                             self.k, st.slot_map, st.slot_stamp, step, self.k if fetch_cap is None else fetch_cap,
-                             copy_local, st.pool_k, st.pool_v, st.moved, stream)
+                             st.scores, self.k, st.slot_map, st.slot_stamp, step,
+                             self.fetch_cap if fetch_cap is None else fetch_cap, copy_local, st.pool_k, st.pool_v,
+                             st.moved, stream)
 
     def refresh_local(self, st: LayerState, ctx_len: torch.Tensor, stream=None):
         """Write the active local block into slot k (stands in for the model's KV write)."""
-        L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, None, None, self.k,
-                             None, None, 0, self.k, True, st.pool_k, st.pool_v, None, stream)
+        L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, None, None, None,
+                             self.k, None, None, 0, self.k, True, st.pool_k, st.pool_v, None, stream)
 
     def attend(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, stream=None):
         L.oasis_sparse_decode_attn(self.dims, q, self.T, st.pool_k, st.pool_v, st.slot_map, self.k, ctx_len,
@@ -160,7 +163,7 @@ class DecodePath:
         pred.wait_event(ev_q)
         if st.ev_staged is not None:
             fg.wait_event(st.ev_staged)
-            pred.wait_event(st.ev_staged)  # the previous transfer of this layer read sel
+            pred.wait_event(st.ev_staged)  # the previous transfer of this layer read sel and scores
         if growing:
             self.refresh_local(st, ctx_len, fg)
         e = tm.begin("attn", fg)
@@ -181,8 +184,8 @@ class DecodePath:
         xfer.wait_event(ev_attn)  # the gather overwrites slots the attention reads
         e = tm.begin("stage", xfer)
         L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, st.sel, st.sel_count,
-                             self.k, st.slot_map, st.slot_stamp, step, self.k, not growing, st.pool_k, st.pool_v,
-                             st.moved if moved is None else moved, xfer)
+                             st.scores, self.k, st.slot_map, st.slot_stamp, step, self.fetch_cap, not growing,
+                             st.pool_k, st.pool_v, st.moved if moved is None else moved, xfer)
         tm.end("stage", xfer, e)
         ev_staged = torch.cuda.Event()
         ev_staged.record(xfer)

@@ -47,7 +47,7 @@ def test_exports_match_header(lib):
 
 
 def test_abi_version(lib):
-    assert lib.oasis_abi_version() == 1
+    assert lib.oasis_abi_version() == 2
 
 
 def test_argument_checks_without_gpu(lib):
@@ -70,12 +70,13 @@ def test_argument_checks_without_gpu(lib):
     big = lib.dims(1, 96, 8, 128, 16, 512)     # G = 12, T = 9 -> 108 attention rows
     assert L.oasis_sparse_decode_attn(ctypes.byref(big), None, 9, None, None, None, 4, None, 1.0, None, None,
                                       None, 0, None) == 2
-    # capped eviction is not implemented yet: explicit UNSUPPORTED
-    assert L.oasis_stage_blocks(ctypes.byref(d), None, None, 10, None, None, None, None, 128, None, None, 0, 6, 1,
-                                None, None, None, None) == 2
+    # a fetch cap below 1 admits nothing and is rejected
+    assert L.oasis_stage_blocks(ctypes.byref(d), None, None, 10, None, None, None, None, None, 128, None, None, 0,
+                                0, 1, None, None, None, None) == 1
+    assert "fetch_cap" in lib.oasis_last_error()
     # local-only form needs copy_local
-    assert L.oasis_stage_blocks(ctypes.byref(d), None, None, 10, None, None, None, None, 128, None, None, 0, 128, 0,
-                                None, None, None, None) == 1
+    assert L.oasis_stage_blocks(ctypes.byref(d), None, None, 10, None, None, None, None, None, 128, None, None, 0,
+                                128, 0, None, None, None, None) == 1
     # zero requests: a no-op that succeeds without touching the device
     z = lib.dims(0, 32, 8, 128, 16, 512)
     assert L.oasis_score_blocks(ctypes.byref(z), None, 5, 1, 4, None, None, None, None, None) == 0

@@ -115,6 +115,42 @@ def test_stage_lru(golden_dir):
         assert np.array_equal(pool_k[0, K, 0], host_k[bt[0, nblocks - 1], 0])
 
 
+def test_stage_capped(golden_dir):
+    g = _load(golden_dir, "stage_capped.json")
+    B, d, nblocks = 2, 4, 32
+    for c in g["cases"]:
+        K = len(c["slot_map"])
+        rng = np.random.default_rng(11)
+        host_k = rng.integers(0, 2 ** 16, size=(nblocks, 1, B, d), dtype=np.uint16)
+        host_v = rng.integers(0, 2 ** 16, size=(nblocks, 1, B, d), dtype=np.uint16)
+        bt = np.arange(nblocks, dtype=np.int32)[::-1].copy()[None, :]
+        ctx = np.array([nblocks * B], dtype=np.int32)
+        sel = np.full((1, 1, K), -1, np.int32)
+        sel[0, 0, :len(c["sel"])] = c["sel"]
+        cnt = np.array([[len(c["sel"])]], np.int32)
+        scores = np.full((1, 1, nblocks), -np.inf)
+        for b, v in c["scores"].items():
+            scores[0, 0, int(b)] = v
+        smap = np.array(c["slot_map"], np.int32)[None, None, :]
+        stamp = np.array(c["slot_stamp"], np.int32)[None, None, :]
+        pool_k = np.zeros((1, K + 1, 1, B, d), np.uint16)
+        pool_v = np.zeros((1, K + 1, 1, B, d), np.uint16)
+        moved = O.stage_blocks(host_k, host_v, bt, sel, cnt, smap, stamp, c["step"], pool_k, pool_v,
+                               ctx, B, copy_local=False, scores=scores, fetch_cap=c["fetch_cap"])
+        assert list(smap[0, 0]) == c["expected_slot_map"]
+        assert list(stamp[0, 0]) == c["expected_slot_stamp"]
+        assert moved[0, 0] == c["expected_moved"]
+        before = c["slot_map"]
+        for s in range(K):
+            b = int(smap[0, 0, s])
+            if b != before[s]:
+                assert np.array_equal(pool_k[0, s, 0], host_k[bt[0, b], 0])
+                assert np.array_equal(pool_v[0, s, 0], host_v[bt[0, b], 0])
+            else:
+                assert not pool_k[0, s, 0].any() and not pool_v[0, s, 0].any()
+        assert not pool_k[0, K].any()
+
+
 def test_attend_sigmoid(golden_dir):
     g = _load(golden_dir, "attend_sigmoid.json")
     keys = f32_to_bf16_bits(np.array(g["keys"], np.float32))

@@ -178,6 +178,46 @@ def test_stage_exact(case, copy_local):
         assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv), step
 
 
+@pytest.mark.parametrize("cap", [1, 3, 17])
+def test_stage_capped_exact(case, cap):
+    """Fetch cap (paper §4.2.3, §5.5.1): admitted misses ranked on the same fp32 scores on both sides."""
+    name, w, hk_t, hv_t = case
+    c = w.cfg
+    d = _dims(w)
+    ctx = w.ctx_len(0)
+    k = c.K
+    n_cand = np.array([O.block_counts(L, c.block_size)[1] for L in ctx])
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap)
+    st = LayerState(d, c.T, k)
+    hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
+    smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
+    stamp = np.zeros_like(smap)
+    pk = np.zeros((c.num_reqs, k + 1, c.num_kv_heads, c.block_size, c.head_dim), np.uint16)
+    pv = np.zeros_like(pk)
+    sel, cnt = random_selection_h(600 + cap, n_cand, c.num_kv_heads, k)
+    ctx_d = dev_i32(ctx)
+    for step in range(1, 7):
+        if step > 1 and step != 4:
+            sel, cnt = random_selection(600 + cap + step, n_cand, k, prev=(sel, cnt), keep_frac=0.7)
+        # ties on every other step: 9 distinct values
+        scores = random_scores(650 + 10 * cap + step, (c.num_reqs, c.num_kv_heads, w.NBmax),
+                               n_distinct=9 if step % 2 else None)
+        moved = O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, step, pk, pv, ctx, c.block_size,
+                               copy_local=True, scores=scores, fetch_cap=cap)
+        note(f"stage capped {name} cap={cap} step={step}")
+        st.sel.copy_(torch.from_numpy(sel))
+        st.sel_count.copy_(torch.from_numpy(cnt))
+        st.scores.copy_(torch.from_numpy(scores))
+        path.stage(st, ctx_d, step)
+        torch.cuda.synchronize()
+        assert np.array_equal(st.slot_map.cpu().numpy(), smap), step
+        assert np.array_equal(st.slot_stamp.cpu().numpy(), stamp), step
+        assert np.array_equal(st.moved.cpu().numpy(), moved), step
+        assert moved.max(initial=0) <= cap
+        assert np.array_equal(host_bits(st.pool_k), pk), step
+        assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv), step
+
+
 def test_stage_local_only(case):
     name, w, hk_t, hv_t = case
     c = w.cfg
@@ -304,8 +344,13 @@ def test_dense_equivalence():
     assert_lse_close(st.lse.cpu().numpy(), ref_l)
 
 
-def test_pipelined_multistep():
-    """Reasoning-style loop: AR(1) queries, one token per step, attention on the previous step's staging."""
+@pytest.mark.parametrize("cap", [None, 2])
+def test_pipelined_multistep(cap):
+    """Reasoning-style loop: AR(1) queries, one token per step, attention on the previous step's staging.
+
+    With a fetch cap, later steps attend stale residents in place of the misses
+    that were not admitted (paper §5.5.1), on both sides alike.
+    """
     steps = 6
     w = make_workload("c3", num_reqs=3, ctx_args=(200, 300, 1400), steps=steps, budget=16 * 24)
     c = w.cfg
@@ -313,7 +358,7 @@ def test_pipelined_multistep():
     hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
     d = _dims(w)
     k = c.K
-    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table))
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap)
     st = LayerState(d, c.T, k)
     smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
     stamp = np.zeros_like(smap)
@@ -331,8 +376,8 @@ def test_pipelined_multistep():
         sc = O.block_scores(q, kmax, kmin, ctx, c.num_kv_heads, c.block_size)
         sel, cnt = O.select_topk(sc, ctx, k, c.block_size)
         moved = O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, s, pk, pv, ctx, c.block_size,
-                               copy_local=False)
-        note(f"pipelined step {s}")
+                               copy_local=False, scores=sc, fetch_cap=cap)
+        note(f"pipelined step {s} cap={cap}")
         ctx_d, q_d = dev_i32(ctx), dev_bf16(q)
         path.build_summaries(st, ctx_d)   # summaries of blocks completed so far
         path.step_pipelined(st, q_d, ctx_d, s, growing=True)
@@ -346,6 +391,8 @@ def test_pipelined_multistep():
         assert np.array_equal(st.moved.cpu().numpy(), moved), s
         if s > 0:
             assert moved.sum() < cnt.sum(), "AR(1) drift: later steps are deltas"
+        if cap is not None:
+            assert moved.max() <= cap
 
 
 # ---------------------------------------------------------------------------
@@ -370,6 +417,6 @@ def test_abi_errors_on_device():
                                 pool, pool)
     with pytest.raises(P.OasisError) as e:
         P.oasis_stage_blocks(d, host.pin_memory(), host.pin_memory(), torch.zeros((1, 16), dtype=torch.int32,
-                             device="cuda"), ctx, smap, torch.zeros((1, 8), dtype=torch.int32, device="cuda"), k,
-                             smap, smap.clone(), 0, k - 1, True, pool, pool, None)
-    assert e.value.status == 2  # capped eviction not implemented yet
+                             device="cuda"), ctx, smap, torch.zeros((1, 8), dtype=torch.int32, device="cuda"), None,
+                             k, smap, smap.clone(), 0, k - 1, True, pool, pool, None)
+    assert e.value.status == 1 and "scores" in str(e.value)  # a binding cap ranks misses by score

@@ -14,7 +14,7 @@ import pytest
 import torch
 
 from oracle import oasis_oracle as O
-from workloads import Config, Workload, f32_to_bf16_bits, make_workload, random_scores
+from workloads import Config, Workload, f32_to_bf16_bits, make_workload, random_scores, random_selection_h
 
 
 def tiny_cfg(**kw):
@@ -296,6 +296,104 @@ def test_stage_cold_idempotent_and_lru():
                 if smap[r, h, s_] in chosen:
                     assert stamp[r, h, s_] == 100
     _check_pool_matches_host(w, hk, hv, smap, pk, pv, ctx)
+
+
+def _random_stage_state(rng, R, H, K, nc):
+    """Slot maps with distinct resident blocks per head, some free slots, random stamps."""
+    smap = np.full((R, H, K), -1, np.int32)
+    for r in range(R):
+        for h in range(H):
+            n_res = int(rng.integers(0, K + 1))
+            slots = rng.choice(K, size=n_res, replace=False)
+            smap[r, h, slots] = rng.choice(nc, size=n_res, replace=False)
+    stamp = rng.integers(0, 6, size=(R, H, K)).astype(np.int32)     # many equal stamps
+    return smap, stamp
+
+
+@pytest.mark.parametrize("cap", [1, 2, 3, 7])
+def test_stage_capped_properties(cap):
+    """Paper §4.2.3 / §5.5.1: at most C pairs per head per step, the rest unchanged.
+
+    Checked against the statement itself, head by head: the admitted misses are
+    exactly the top-C misses by (score, -id) (brute force over all misses), the
+    slots that change are exactly the first victims in LRU order, every other
+    slot keeps its block and stamp, and a cap that does not bind reproduces the
+    uncapped plan bit for bit.
+    """
+    rng = np.random.default_rng(100 + cap)
+    R, H, K, B, d, nc = 3, 4, 8, 2, 4, 24
+    hk = rng.integers(0, 2 ** 16, size=(nc + 1, H, B, d), dtype=np.uint16)
+    hv = rng.integers(0, 2 ** 16, size=(nc + 1, H, B, d), dtype=np.uint16)
+    bt = np.stack([rng.permutation(nc + 1) for _ in range(R)]).astype(np.int32)
+    ctx = np.full(R, (nc + 1) * B, np.int32)
+    scores = random_scores(31 + cap, (R, H, nc + 1), n_distinct=6)     # many exact ties
+    for trial in range(4):
+        smap, stamp = _random_stage_state(rng, R, H, K, nc)
+        sel, cnt = random_selection_h(1000 * cap + trial, np.full(R, nc), H, K)
+        pk = np.zeros((R, K + 1, H, B, d), np.uint16)
+        pv = np.zeros_like(pk)
+        m0, s0 = smap.copy(), stamp.copy()
+        um, us = smap.copy(), stamp.copy()
+        upk, upv = pk.copy(), pv.copy()
+        O.stage_blocks(hk, hv, bt, sel, cnt, um, us, 9, upk, upv, ctx, B, copy_local=False)
+        moved = O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, 9, pk, pv, ctx, B, copy_local=False,
+                               scores=scores, fetch_cap=cap)
+        for r in range(R):
+            for h in range(H):
+                chosen = [int(b) for b in sel[r, h, :cnt[r, h]]]
+                resident = {int(b) for b in m0[r, h] if b >= 0}
+                misses = [b for b in chosen if b not in resident]
+                n_adm = min(cap, len(misses))
+                assert moved[r, h] == n_adm
+                admitted = {int(smap[r, h, s]) for s in range(K) if smap[r, h, s] != m0[r, h, s]}
+                assert len(admitted) == n_adm and admitted <= set(misses)
+                key = lambda b: (float(scores[r, h, b]), -b)
+                for b in set(misses) - admitted:                    # nothing left out beats anything admitted
+                    assert all(key(b) < key(a) for a in admitted)
+                free = [s for s in range(K) if m0[r, h, s] < 0]
+                stale = sorted((int(s0[r, h, s]), s) for s in range(K)
+                               if m0[r, h, s] >= 0 and m0[r, h, s] not in chosen)
+                victims = free + [s for _, s in stale]
+                changed = sorted(s for s in range(K) if smap[r, h, s] != m0[r, h, s])
+                assert changed == sorted(victims[:n_adm])
+                for s in range(K):
+                    b = int(smap[r, h, s])
+                    if b in chosen:
+                        assert stamp[r, h, s] == 9
+                    else:
+                        assert b == m0[r, h, s] and stamp[r, h, s] == s0[r, h, s]
+                    if s in changed:
+                        assert np.array_equal(pk[r, s, h], hk[bt[r, b], h])
+                        assert np.array_equal(pv[r, s, h], hv[bt[r, b], h])
+                if len(misses) <= cap:
+                    assert np.array_equal(smap[r, h], um[r, h]) and np.array_equal(stamp[r, h], us[r, h])
+
+
+def test_stage_capped_converges():
+    """With a fixed selection, a cap of C fills n misses in ceil(n / C) steps (§4.2.3)."""
+    rng = np.random.default_rng(5)
+    R, H, K, B, d, nc = 2, 2, 12, 2, 4, 40
+    hk = rng.integers(0, 2 ** 16, size=(nc, H, B, d), dtype=np.uint16)
+    hv = rng.integers(0, 2 ** 16, size=(nc, H, B, d), dtype=np.uint16)
+    bt = np.stack([rng.permutation(nc) for _ in range(R)]).astype(np.int32)
+    ctx = np.full(R, nc * B + 1, np.int32)                     # block nc is the local block
+    scores = random_scores(8, (R, H, nc + 1))
+    sel, cnt = random_selection_h(9, np.full(R, nc), H, K)
+    for cap in (1, 5, 12):
+        smap, stamp, pk, pv = (np.full((R, H, K), -1, np.int32), np.zeros((R, H, K), np.int32),
+                               np.zeros((R, K + 1, H, B, d), np.uint16), np.zeros((R, K + 1, H, B, d), np.uint16))
+        steps = math.ceil(K / cap)
+        total = 0
+        for t in range(steps):
+            moved = O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, t, pk, pv, ctx, B, copy_local=False,
+                                   scores=scores, fetch_cap=cap)
+            total += moved
+            if t < steps - 1:
+                assert (smap < 0).any(axis=2).all()
+        assert np.array_equal(total, np.full((R, H), K))
+        for r in range(R):
+            for h in range(H):
+                assert sorted(smap[r, h]) == sorted(sel[r, h, :cnt[r, h]])
 
 
 # ---------------------------------------------------------------------------

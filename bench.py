@@ -29,6 +29,13 @@ import time
 
 import numpy as np
 
+# The pipelined step keeps three streams busy at once (foreground, prediction,
+# transfer). With HIP's default of 4 hardware queues per process the runtime
+# can place two of them on one queue, where each serializes behind the other's
+# waits (measured: about 1 process in 6 ran 2.5x slower). More queues give every
+# stream its own; this must be set before HIP initializes.
+os.environ.setdefault("GPU_MAX_HW_QUEUES", "16")
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
@@ -71,8 +78,14 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes": n, "dispatches": 3}), flush=True)
 
 
-def cpu_baseline(w, hk, hv, q0, k, budget_s):
-    """Time the oracle on a bounded sample: whole requests of the same workload."""
+def cpu_baseline(w, hk, hv, queries, k, fetch_cap, budget_s):
+    """Time the oracle on a bounded sample of the same step.
+
+    Every request's working set is first filled from its step-0 prediction
+    (untimed, as on the GPU); then whole-batch decode steps are timed, each
+    one scoring, top-K, capped delta staging and attention per request, until
+    the budget is spent. ``queries`` are the bf16 queries of consecutive steps.
+    """
     from oracle import oasis_oracle as O
     try:
         from threadpoolctl import threadpool_limits
@@ -81,31 +94,37 @@ def cpu_baseline(w, hk, hv, q0, k, budget_s):
     import contextlib
     c = w.cfg
     ctx = w.ctx_len(0)
-    done, spent = 0, 0.0
+    B, H, d = c.block_size, c.num_kv_heads, c.head_dim
+    cap = None if fetch_cap >= k else fetch_cap
     limit = threadpool_limits(limits=1) if threadpool_limits is not None else contextlib.nullcontext()
     with limit:
-        for r in range(c.num_reqs):
-            bt = w.block_table[r:r + 1]
-            cr = ctx[r:r + 1]
-            qr = q0[r:r + 1]
-            kmax, kmin = O.block_summaries(hk, bt, cr, c.block_size, w.NBmax)   # setup, not timed
-            t0 = time.perf_counter()
-            s = O.block_scores(qr, kmax, kmin, cr, c.num_kv_heads, c.block_size)
-            sel, cnt = O.select_topk(s, cr, k, c.block_size)
-            smap = np.full((1, c.num_kv_heads, k), -1, np.int32)
-            pk = np.zeros((1, k + 1, c.num_kv_heads, c.block_size, c.head_dim), np.uint16)
+        state = []
+        for r in range(c.num_reqs):   # setup, not timed
+            bt, cr = w.block_table[r:r + 1], ctx[r:r + 1]
+            kmax, kmin = O.block_summaries(hk, bt, cr, B, w.NBmax)
+            s = O.block_scores(queries[0][r:r + 1], kmax, kmin, cr, H, B)
+            sel, cnt = O.select_topk(s, cr, k, B)
+            smap = np.full((1, H, k), -1, np.int32)
+            stamp = np.zeros_like(smap)
+            pk = np.zeros((1, k + 1, H, B, d), np.uint16)
             pv = np.zeros_like(pk)
-            O.stage_blocks(hk, hv, bt, sel, cnt, smap, np.zeros_like(smap), 0, pk, pv, cr, c.block_size)
-            O.sparse_attend(qr, pk, pv, smap, cr, c.block_size)
-            spent += time.perf_counter() - t0
-            done += 1
-            if spent >= budget_s:
-                break
-    per_step_s = spent / done * c.num_reqs
-    return {"value": 1.0 / per_step_s, "unit": "steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done} of {c.num_reqs} requests (all {c.num_kv_heads} KV heads each): scores, top-K, "
-                      f"cold staging and attention in float64 NumPy on 1 thread, {spent:.1f} s, scaled to the "
-                      f"full batch"}
+            O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, 0, pk, pv, cr, B)
+            state.append((bt, cr, kmax, kmin, smap, stamp, pk, pv))
+        steps, spent = 0, 0.0
+        while spent < budget_s and steps + 1 < len(queries):
+            steps += 1
+            for r, (bt, cr, kmax, kmin, smap, stamp, pk, pv) in enumerate(state):
+                qr = queries[steps][r:r + 1]
+                t0 = time.perf_counter()
+                s = O.block_scores(qr, kmax, kmin, cr, H, B)
+                sel, cnt = O.select_topk(s, cr, k, B)
+                O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, steps, pk, pv, cr, B, scores=s, fetch_cap=cap)
+                O.sparse_attend(qr, pk, pv, smap, cr, B)
+                spent += time.perf_counter() - t0
+    return {"value": steps / spent, "unit": "steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"{steps} whole decode steps of all {c.num_reqs} requests (scores, top-K, delta staging "
+                      f"with fetch cap {fetch_cap}, attention; after an untimed initial fill) in float64 NumPy "
+                      f"on 1 thread, {spent:.1f} s"}
 
 
 def main():
@@ -122,7 +141,7 @@ def main():
     import torch
 
     import paper_2608_08097_amd as P
-    from paper_2608_08097_amd.path import DecodePath, KernelTimer
+    from paper_2608_08097_amd.path import DecodePath
     from workloads import config, Workload
 
     if not os.path.exists(P._lib.LIB_PATH):
@@ -167,37 +186,36 @@ def main():
     moved_log = torch.zeros((args.steps, c.num_reqs, c.num_kv_heads), dtype=torch.int32, device="cuda")
     torch.cuda.synchronize()
 
-    timer = KernelTimer()
-
-    def run(i, timed, with_events):
+    def run(i, timed):
         l, s = i % NL, i // NL
-        path.step_pipelined(layers[l], qs[l][s], ctx_d, i, growing=False, timer=timer if with_events else None,
+        path.step_pipelined(layers[l], qs[l][s], ctx_d, i, growing=False,
                             moved=moved_log[(i - args.warmup) % args.steps] if timed else None)
 
     for i in range(args.warmup):
-        run(i, False, False)
+        run(i, False)
     path.join()
     torch.cuda.synchronize()
     log(f"warmup {args.warmup} steps done")
     # Timed region 1: the step rate (no events between kernels).
     t_start = time.perf_counter()
     for i in range(args.warmup, total_steps):
-        run(i, True, False)
+        run(i, True)
     path.join()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     ms_per_step = 1000.0 * elapsed / args.steps
     log(f"timed {args.steps} steps in {elapsed:.3f} s")
-    # Timed region 2: the same steps again with HIP events around every kernel,
-    # recorded on the stream the kernel runs on (per-kernel durations).
+    # Timed region 2: the same pipelined steps again with HIP timing events
+    # recorded by the native issuer around every kernel, on the stream the
+    # kernel runs on (per-kernel durations inside the running pipeline).
     moved_rate = moved_log.cpu().numpy().copy()
+    path.profile_begin(args.steps)
     for i in range(total_steps, total_steps + args.steps):
-        run(i, False, True)
+        run(i, False)
     path.join()
     torch.cuda.synchronize()
-
-    # per-kernel averages (HIP events on each kernel's stream)
-    us = {k_: timer.mean_us(k_) for k_ in ("score", "topk", "stage", "attn")}
+    us, n_prof = path.profile_end()
+    assert n_prof == args.steps
     n_cand = np.array([max(0, (int(L) + c.block_size - 1) // c.block_size - 1) for L in ctx])
     bh = int(n_cand.sum()) * c.num_kv_heads                      # candidate block-heads per step
     score_bytes = bh * (2 * c.head_dim * 2) + c.num_reqs * c.num_kv_heads * w.NBmax * 4 \
@@ -254,9 +272,8 @@ def main():
     if args.isolated:
         result["isolated"] = isolated(P, torch, path, layers, qs, ctx_d, score_bytes, attn_bytes)
     if not args.no_cpu_baseline:
-        q0 = w.layer_queries(0, 1)[0]
         log("timing the oracle sample")
-        result["cpu_baseline"] = cpu_baseline(w, hk, hv, q0, K, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(w, hk, hv, w.layer_queries(0, 64), K, fetch_cap, args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 

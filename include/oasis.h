@@ -215,6 +215,96 @@ OASIS_API oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const ui
                                       float scale, uint16_t* out, float* lse,
                                       void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Native step issuer for the layer-pipelined schedule (paper §4.2.2, the
+ * asynchronous prefetch pipeline figure and Eq. "prefetch-rate"; §5.1: the
+ * stages run on background streams and events order each layer's chain).
+ * One oasis_pipeline_step call issues one layer's decode step on three HIP
+ * streams:
+ *   foreground (`stream`): wait for this layer's transfer issued at its
+ *     previous step (a layer-local wait, not a wait for every layer), refresh
+ *     the local block if `growing`, then oasis_sparse_decode_attn over the
+ *     working set;
+ *   prediction stream: once q is ready and the layer's previous transfer has
+ *     read sel and scores, oasis_score_blocks on the draft rows of q and
+ *     oasis_select_topk (the prediction for the layer's next step);
+ *   transfer stream: once the prediction is ready and this step's attention
+ *     has read the pools, oasis_stage_blocks (delta selection with the fetch
+ *     cap, then the gather; the paper's selection and transfer stages are one
+ *     kernel here), with copy_local = !growing.
+ * Consecutive calls for different layers overlap one layer's transfer with
+ * the next layers' attention and prediction. The streams are ordered through
+ * monotone counters in device memory (stream write-value after the producer,
+ * stream wait-value before the consumer): four such edges and five or six
+ * kernel launches per step, nothing allocated.
+ *
+ * Arguments are checked on every step exactly as the four entry points check
+ * them. Ownership: every pointer stays the caller's and must outlive the
+ * pipeline's use of it (tensors read by a step stay alive until the layer's
+ * next step or a join); the pipeline owns its counter array (hipMalloc at
+ * create, 256 bytes per counter, (5 + max_layers) counters) and the two
+ * background streams when it creates them. host_k/host_v are resolved to
+ * device-visible addresses once, at create. All calls for one pipeline must come
+ * from one host thread with the creating device current.
+ */
+typedef struct oasis_pipeline oasis_pipeline;
+
+/* Per-layer device buffers of the path (shapes as in the entry points above). */
+typedef struct {
+  uint16_t* kmax;          /* bf16 [R][Hkv][max_blocks][d] (oasis_build_summaries) */
+  uint16_t* kmin;
+  float* scores;           /* [R][Hkv][max_blocks] */
+  int32_t* sel;            /* [R][Hkv][k] */
+  int32_t* sel_count;      /* [R][Hkv] */
+  int32_t* slot_map;       /* [R][Hkv][k], -1 = free */
+  int32_t* slot_stamp;     /* [R][Hkv][k] */
+  uint16_t* pool_k;        /* bf16 [R][k+1][Hkv][B][d] */
+  uint16_t* pool_v;        /* bf16 [R][k+1][Hkv][d][B] */
+  int32_t* moved;          /* [R][Hkv], nullable */
+  uint16_t* out;           /* bf16 [R][T][Hq][d] */
+  float* lse;              /* [R][T][Hq], nullable */
+  void* workspace;         /* oasis_attn_workspace_bytes(dims, T, k) bytes */
+  size_t workspace_bytes;
+} oasis_layer_buffers;
+
+/* pred_stream / xfer_stream: caller streams (non-blocking, default priority) or
+ * NULL to let the pipeline create its own. max_layers >= 1 bounds the layer ids
+ * of set_layer / step. fetch_cap as in oasis_stage_blocks (>= k: uncapped). */
+OASIS_API oasis_status oasis_pipeline_create(const oasis_dims* dims, int32_t num_q_tokens, int32_t first_draft,
+                                   int32_t num_draft, int32_t k, int32_t fetch_cap, float scale,
+                                   const uint16_t* host_k, const uint16_t* host_v, int64_t num_pages,
+                                   const int32_t* host_block_table, int32_t max_layers, void* pred_stream,
+                                   void* xfer_stream, oasis_pipeline** pipeline);
+
+/* Register (or replace) the buffers of layer `layer` (0 <= layer < max_layers). A
+ * transfer already issued for the layer is still waited on at its next step. */
+OASIS_API oasis_status oasis_pipeline_set_layer(oasis_pipeline* pipeline, int32_t layer,
+                                      const oasis_layer_buffers* buffers);
+
+/* Issue one decode step of `layer` (see above). q: bf16 device [R][T][Hq][d];
+ * ctx_len: device [R]; step: the stamp of this step's selection; moved: where
+ * the transfer writes its per-(r, h) entry counts (NULL: the layer's buffer). */
+OASIS_API oasis_status oasis_pipeline_step(oasis_pipeline* pipeline, int32_t layer, const uint16_t* q,
+                                 const int32_t* ctx_len, int32_t step, int32_t growing, int32_t* moved,
+                                 void* stream);
+
+/* Make `stream` wait for all work issued so far on the two background streams. */
+OASIS_API oasis_status oasis_pipeline_join(oasis_pipeline* pipeline, void* stream);
+
+/* Profile the next max_steps steps: timing events are recorded around each
+ * kernel on the stream it runs on (attention incl. its merge on the foreground;
+ * scoring and top-K on the prediction stream; staging on the transfer stream).
+ * The events are created here, not in the steps. */
+OASIS_API oasis_status oasis_pipeline_profile_begin(oasis_pipeline* pipeline, int32_t max_steps);
+
+/* Wait for the profiled steps and write the mean duration in microseconds of
+ * attention, scoring, top-K and staging to avg_us[0..3] (steps: how many steps
+ * were profiled, nullable); releases the profile's events. */
+OASIS_API oasis_status oasis_pipeline_profile_end(oasis_pipeline* pipeline, float* avg_us, int32_t* steps);
+
+/* Synchronize the device, then release the counters (and owned streams). NULL is a no-op. */
+OASIS_API void oasis_pipeline_destroy(oasis_pipeline* pipeline);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,6 +24,8 @@ EXPORTS = (
     "oasis_last_error", "oasis_abi_version", "oasis_build_summaries", "oasis_score_blocks",
     "oasis_select_topk", "oasis_stage_blocks",
     "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn",
+    "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_step", "oasis_pipeline_join",
+    "oasis_pipeline_destroy", "oasis_pipeline_profile_begin", "oasis_pipeline_profile_end",
 )
 
 
@@ -40,6 +42,12 @@ class OasisDims(ctypes.Structure):
 
     def __repr__(self):
         return "OasisDims(" + ", ".join(f"{n}={getattr(self, n)}" for n, _ in self._fields_) + ")"
+
+
+class OasisLayerBuffers(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("kmax", "kmin", "scores", "sel", "sel_count", "slot_map",
+                                               "slot_stamp", "pool_k", "pool_v", "moved", "out", "lse",
+                                               "workspace")] + [("workspace_bytes", ctypes.c_size_t)]
 
 
 def dims(num_reqs, num_q_heads, num_kv_heads, head_dim, block_size, max_blocks) -> OasisDims:
@@ -82,6 +90,21 @@ def lib() -> ctypes.CDLL:
         L.oasis_sparse_decode_attn.restype = _I32
         L.oasis_sparse_decode_attn.argtypes = [_DIMS, _P, _I32, _P, _P, _P, _I32, _P, ctypes.c_float, _P, _P,
                                                _P, _SZ, _P]
+        L.oasis_pipeline_create.restype = _I32
+        L.oasis_pipeline_create.argtypes = [_DIMS, _I32, _I32, _I32, _I32, _I32, ctypes.c_float, _P, _P, _I64, _P,
+                                            _I32, _P, _P, ctypes.POINTER(_P)]
+        L.oasis_pipeline_set_layer.restype = _I32
+        L.oasis_pipeline_set_layer.argtypes = [_P, _I32, ctypes.POINTER(OasisLayerBuffers)]
+        L.oasis_pipeline_step.restype = _I32
+        L.oasis_pipeline_step.argtypes = [_P, _I32, _P, _P, _I32, _I32, _P, _P]
+        L.oasis_pipeline_join.restype = _I32
+        L.oasis_pipeline_join.argtypes = [_P, _P]
+        L.oasis_pipeline_destroy.restype = None
+        L.oasis_pipeline_destroy.argtypes = [_P]
+        L.oasis_pipeline_profile_begin.restype = _I32
+        L.oasis_pipeline_profile_begin.argtypes = [_P, _I32]
+        L.oasis_pipeline_profile_end.restype = _I32
+        L.oasis_pipeline_profile_end.argtypes = [_P, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_I32)]
         _lib = L
     return _lib
 
@@ -228,3 +251,87 @@ def oasis_sparse_decode_attn(d: OasisDims, q, num_q_tokens: int, pool_k, pool_v,
         _dev(ctx_len, "ctx_len", _I32T), float(scale), _dev(out, "out", _BF16),
         _dev(lse, "lse", _F32, nullable=True), _dev(workspace, "workspace", (torch.uint8,)),
         int(workspace.numel()), _stream(stream)))
+
+
+# --- native step issuer --------------------------------------------------------
+
+_PIPE_SIZES: dict[int, tuple[int, int, int]] = {}  # handle -> element counts of q, ctx_len, moved
+
+def oasis_pipeline_create(d: OasisDims, num_q_tokens: int, first_draft: int, num_draft: int, k: int,
+                          fetch_cap: int, scale: float | None, host_k, host_v, host_block_table, max_layers: int,
+                          pred_stream=None, xfer_stream=None) -> int:
+    """Returns the pipeline handle (an address); release it with oasis_pipeline_destroy."""
+    if scale is None:
+        scale = 1.0 / math.sqrt(d.head_dim)
+    if host_k.shape != host_v.shape:
+        raise ValueError("host_k and host_v differ in shape")
+    _need(host_k, host_k.shape[0] * d.num_kv_heads * d.block_size * d.head_dim, "host_k")
+    _need(host_block_table, d.num_reqs * d.max_blocks, "host_block_table")
+    h = ctypes.c_void_p()
+    _check("oasis_pipeline_create", lib().oasis_pipeline_create(
+        ctypes.byref(d), int(num_q_tokens), int(first_draft), int(num_draft), int(k), int(fetch_cap), float(scale),
+        _host_or_dev(host_k, "host_k", _BF16), _host_or_dev(host_v, "host_v", _BF16), int(host_k.shape[0]),
+        _dev(host_block_table, "host_block_table", _I32T),
+        int(max_layers), None if pred_stream is None else _stream(pred_stream),
+        None if xfer_stream is None else _stream(xfer_stream), ctypes.byref(h)))
+    _PIPE_SIZES[h.value] = (d.num_reqs * int(num_q_tokens) * d.num_q_heads * d.head_dim, d.num_reqs,
+                            d.num_reqs * d.num_kv_heads)
+    return h.value
+
+
+def oasis_pipeline_set_layer(handle: int, layer: int, d: OasisDims, num_q_tokens: int, k: int, kmax, kmin, scores,
+                             sel, sel_count, slot_map, slot_stamp, pool_k, pool_v, moved, out, lse,
+                             workspace) -> None:
+    R, H, NB, D, B = d.num_reqs, d.num_kv_heads, d.max_blocks, d.head_dim, d.block_size
+    T, Hq = int(num_q_tokens), d.num_q_heads
+    for t, n, name in ((kmax, R * H * NB * D, "kmax"), (kmin, R * H * NB * D, "kmin"), (scores, R * H * NB, "scores"),
+                       (sel, R * H * k, "sel"), (sel_count, R * H, "sel_count"), (slot_map, R * H * k, "slot_map"),
+                       (slot_stamp, R * H * k, "slot_stamp"), (pool_k, R * (k + 1) * H * B * D, "pool_k"),
+                       (pool_v, R * (k + 1) * H * B * D, "pool_v"), (moved, R * H, "moved"),
+                       (out, R * T * Hq * D, "out"), (lse, R * T * Hq, "lse")):
+        _need(t, n, name)
+    b = OasisLayerBuffers(
+        _dev(kmax, "kmax", _BF16), _dev(kmin, "kmin", _BF16), _dev(scores, "scores", _F32),
+        _dev(sel, "sel", _I32T), _dev(sel_count, "sel_count", _I32T), _dev(slot_map, "slot_map", _I32T),
+        _dev(slot_stamp, "slot_stamp", _I32T), _dev(pool_k, "pool_k", _BF16), _dev(pool_v, "pool_v", _BF16),
+        _dev(moved, "moved", _I32T, nullable=True), _dev(out, "out", _BF16), _dev(lse, "lse", _F32, nullable=True),
+        _dev(workspace, "workspace", (torch.uint8,), nullable=True),
+        0 if workspace is None else workspace.numel() * workspace.element_size())
+    _check("oasis_pipeline_set_layer", lib().oasis_pipeline_set_layer(handle, int(layer), ctypes.byref(b)))
+
+
+def oasis_pipeline_step(handle: int, layer: int, q, ctx_len, step: int, growing: bool, moved=None,
+                        stream=None) -> None:
+    """One layer's pipelined step (q, ctx_len, moved: device tensors of the pipeline's shapes)."""
+    nq, nr, nm = _PIPE_SIZES[handle]
+    _need(q, nq, "q")
+    _need(ctx_len, nr, "ctx_len")
+    _need(moved, nm, "moved")
+    _check("oasis_pipeline_step", lib().oasis_pipeline_step(
+        handle, int(layer), _dev(q, "q", _BF16), _dev(ctx_len, "ctx_len", _I32T), int(step), 1 if growing else 0,
+        _dev(moved, "moved", _I32T, nullable=True), _stream(stream)))
+
+
+def oasis_pipeline_join(handle: int, stream=None) -> None:
+    _check("oasis_pipeline_join", lib().oasis_pipeline_join(handle, _stream(stream)))
+
+
+def oasis_pipeline_destroy(handle: int | None) -> None:
+    if handle:
+        _PIPE_SIZES.pop(handle, None)
+        lib().oasis_pipeline_destroy(handle)
+
+
+PROFILE_KINDS = ("attn", "score", "topk", "stage")
+
+
+def oasis_pipeline_profile_begin(handle: int, max_steps: int) -> None:
+    _check("oasis_pipeline_profile_begin", lib().oasis_pipeline_profile_begin(handle, int(max_steps)))
+
+
+def oasis_pipeline_profile_end(handle: int) -> tuple[dict[str, float], int]:
+    """Mean kernel durations (us) over the profiled steps, and the number of steps."""
+    avg = (ctypes.c_float * 4)()
+    n = _I32()
+    _check("oasis_pipeline_profile_end", lib().oasis_pipeline_profile_end(handle, avg, ctypes.byref(n)))
+    return {k: float(avg[i]) for i, k in enumerate(PROFILE_KINDS)}, int(n.value)

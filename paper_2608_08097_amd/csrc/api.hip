@@ -1,14 +1,20 @@
 // C ABI of the OasisKV decode path: argument checks, workspace carving and
 // kernel launches. Nothing here allocates memory or throws.
+//
+// Every entry point is "check and build the kernel arguments" followed by one
+// launch; the builders are shared with the native step issuer (pipeline.hip),
+// so both forms accept and reject exactly the same arguments.
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 
 #include "oasis_internal.h"
 
-namespace {
+namespace oasis {
 
+namespace {
 thread_local char g_err[512] = "";
+}  // namespace
 
 oasis_status fail(oasis_status st, const char* fmt, ...) {
   va_list ap;
@@ -23,6 +29,8 @@ oasis_status ok() {
   return OASIS_OK;
 }
 
+const char* last_error() { return g_err; }
+
 oasis_status hip_status(hipError_t e, const char* where) {
   if (e == hipSuccess) return ok();
   return fail(OASIS_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
@@ -36,7 +44,7 @@ oasis_status check_dims(const oasis_dims* d, const char* fn) {
   if (d->num_q_heads % d->num_kv_heads)
     return fail(OASIS_ERR_INVALID_ARG, "%s: num_q_heads (%d) is not a multiple of num_kv_heads (%d)", fn,
                 d->num_q_heads, d->num_kv_heads);
-  if (d->head_dim != oasis::kHeadDim)
+  if (d->head_dim != kHeadDim)
     return fail(OASIS_ERR_UNSUPPORTED, "%s: head_dim %d (only 128 is supported)", fn, d->head_dim);
   if (d->block_size != 16 && d->block_size != 32)
     return fail(OASIS_ERR_UNSUPPORTED, "%s: block_size %d (16 or 32 are supported)", fn, d->block_size);
@@ -51,7 +59,6 @@ oasis_status check_dims(const oasis_dims* d, const char* fn) {
     if (!(p)) return fail(OASIS_ERR_INVALID_ARG, "%s: " #p " is NULL", fn); \
   } while (0)
 
-// Device-visible address of pinned host memory (or of device memory as is).
 oasis_status device_view(const void* p, const void** out, const char* what, const char* fn) {
   hipPointerAttribute_t attr;
   const hipError_t e = hipPointerGetAttributes(&attr, p);
@@ -71,39 +78,9 @@ oasis_status device_view(const void* p, const void** out, const char* what, cons
   return fail(OASIS_ERR_INVALID_ARG, "%s: %s is host memory that is not pinned and mapped", fn, what);
 }
 
-}  // namespace
-
-extern "C" {
-
-const char* oasis_last_error(void) { return g_err; }
-
-int32_t oasis_abi_version(void) { return OASIS_ABI_VERSION; }
-
-oasis_status oasis_build_summaries(const oasis_dims* dims, const uint16_t* k_pages, int64_t num_pages,
-                                   const int32_t* block_table, const int32_t* ctx_len, uint16_t* kmax,
-                                   uint16_t* kmin, void* stream) {
-  static const char* fn = "oasis_build_summaries";
-  oasis_status st = check_dims(dims, fn);
-  if (st != OASIS_OK) return st;
-  if (dims->num_reqs == 0) return ok();
-  REQUIRE_PTR(k_pages, fn);
-  REQUIRE_PTR(block_table, fn);
-  REQUIRE_PTR(ctx_len, fn);
-  REQUIRE_PTR(kmax, fn);
-  REQUIRE_PTR(kmin, fn);
-  if (num_pages < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: num_pages < 1", fn);
-  const void* kp = nullptr;
-  st = device_view(k_pages, &kp, "k_pages", fn);
-  if (st != OASIS_OK) return st;
-  oasis::SummaryArgs a{static_cast<const uint16_t*>(kp), num_pages, block_table, ctx_len, kmax, kmin,
-                       dims->num_reqs, dims->num_kv_heads, dims->block_size, dims->max_blocks};
-  return hip_status(oasis::launch_summaries(a, static_cast<hipStream_t>(stream)), fn);
-}
-
-oasis_status oasis_score_blocks(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens,
-                                int32_t first_draft, int32_t num_draft, const uint16_t* kmax,
-                                const uint16_t* kmin, const int32_t* ctx_len, float* scores, void* stream) {
-  static const char* fn = "oasis_score_blocks";
+oasis_status make_score_args(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens, int32_t first_draft,
+                             int32_t num_draft, const uint16_t* kmax, const uint16_t* kmin, const int32_t* ctx_len,
+                             float* scores, ScoreArgs* a, const char* fn) {
   oasis_status st = check_dims(dims, fn);
   if (st != OASIS_OK) return st;
   if (num_q_tokens < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: num_q_tokens < 1", fn);
@@ -114,40 +91,40 @@ oasis_status oasis_score_blocks(const oasis_dims* dims, const uint16_t* q, int32
   if ((long long)num_draft * G > 64)
     return fail(OASIS_ERR_UNSUPPORTED, "%s: num_draft * G = %lld scoring rows (at most 64)", fn,
                 (long long)num_draft * G);
-  if (dims->num_reqs == 0) return ok();
+  if (dims->num_reqs == 0) return OASIS_OK;
   REQUIRE_PTR(q, fn);
   REQUIRE_PTR(kmax, fn);
   REQUIRE_PTR(kmin, fn);
   REQUIRE_PTR(ctx_len, fn);
   REQUIRE_PTR(scores, fn);
-  oasis::ScoreArgs a{q, kmax, kmin, ctx_len, scores, dims->num_reqs, dims->num_q_heads, dims->num_kv_heads, G,
-                     num_q_tokens, first_draft, num_draft, dims->block_size, dims->max_blocks};
-  return hip_status(oasis::launch_score(a, static_cast<hipStream_t>(stream)), fn);
+  *a = ScoreArgs{q, kmax, kmin, ctx_len, scores, dims->num_reqs, dims->num_q_heads, dims->num_kv_heads, G,
+                 num_q_tokens, first_draft, num_draft, dims->block_size, dims->max_blocks};
+  return OASIS_OK;
 }
 
-oasis_status oasis_select_topk(const oasis_dims* dims, const float* scores, const int32_t* ctx_len, int32_t k,
-                               int32_t* sel, int32_t* sel_count, void* stream) {
-  static const char* fn = "oasis_select_topk";
+oasis_status make_topk_args(const oasis_dims* dims, const float* scores, const int32_t* ctx_len, int32_t k,
+                            int32_t* sel, int32_t* sel_count, TopkArgs* a, const char* fn) {
   oasis_status st = check_dims(dims, fn);
   if (st != OASIS_OK) return st;
   if (k < 1 || k > 65536) return fail(OASIS_ERR_INVALID_ARG, "%s: k = %d outside [1, 65536]", fn, k);
-  if (dims->num_reqs == 0) return ok();
+  if (dims->num_reqs == 0) return OASIS_OK;
   REQUIRE_PTR(scores, fn);
   REQUIRE_PTR(ctx_len, fn);
   REQUIRE_PTR(sel, fn);
   REQUIRE_PTR(sel_count, fn);
-  oasis::TopkArgs a{scores, ctx_len, sel, sel_count, dims->num_reqs, dims->num_kv_heads, dims->block_size,
-                    dims->max_blocks, k};
-  return hip_status(oasis::launch_topk(a, static_cast<hipStream_t>(stream)), fn);
+  *a = TopkArgs{scores, ctx_len, sel, sel_count, dims->num_reqs, dims->num_kv_heads, dims->block_size,
+                dims->max_blocks, k};
+  return OASIS_OK;
 }
 
-oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, const uint16_t* host_v,
-                                int64_t num_pages, const int32_t* host_block_table, const int32_t* ctx_len,
-                                const int32_t* sel, const int32_t* sel_count, const float* scores, int32_t k,
-                                int32_t* slot_map,
-                                int32_t* slot_stamp, int32_t step, int32_t fetch_cap, int32_t copy_local,
-                                uint16_t* pool_k, uint16_t* pool_v, int32_t* moved, void* stream) {
-  static const char* fn = "oasis_stage_blocks";
+// host_k / host_v are stored as given: the caller passes device-visible addresses
+// (device_view) before launching.
+oasis_status make_stage_args(const oasis_dims* dims, const uint16_t* host_k, const uint16_t* host_v,
+                             int64_t num_pages, const int32_t* host_block_table, const int32_t* ctx_len,
+                             const int32_t* sel, const int32_t* sel_count, const float* scores, int32_t k,
+                             int32_t* slot_map, int32_t* slot_stamp, int32_t step, int32_t fetch_cap,
+                             int32_t copy_local, uint16_t* pool_k, uint16_t* pool_v, int32_t* moved, StageArgs* a,
+                             const char* fn) {
   oasis_status st = check_dims(dims, fn);
   if (st != OASIS_OK) return st;
   if (k < 1 || k > 1024) return fail(OASIS_ERR_INVALID_ARG, "%s: k = %d outside [1, 1024]", fn, k);
@@ -159,7 +136,7 @@ oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, 
   const bool local_only = sel == nullptr;
   if (local_only && !copy_local)
     return fail(OASIS_ERR_INVALID_ARG, "%s: no selection and copy_local = 0: nothing to do", fn);
-  if (dims->num_reqs == 0) return ok();
+  if (dims->num_reqs == 0) return OASIS_OK;
   REQUIRE_PTR(host_k, fn);
   REQUIRE_PTR(host_v, fn);
   REQUIRE_PTR(host_block_table, fn);
@@ -171,37 +148,164 @@ oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, 
     REQUIRE_PTR(slot_stamp, fn);
     if (fetch_cap < k) REQUIRE_PTR(scores, fn);
   }
-  const void *hk = nullptr, *hv = nullptr;
-  if ((st = device_view(host_k, &hk, "host_k", fn)) != OASIS_OK) return st;
-  if ((st = device_view(host_v, &hv, "host_v", fn)) != OASIS_OK) return st;
+  StageArgs s{};
+  s.host_k = host_k;
+  s.host_v = host_v;
+  s.num_pages = num_pages;
+  s.block_table = host_block_table;
+  s.ctx_len = ctx_len;
+  s.sel = sel;
+  s.sel_count = sel_count;
+  s.scores = scores;
+  s.slot_map = slot_map;
+  s.slot_stamp = slot_stamp;
+  s.pool_k = pool_k;
+  s.pool_v = pool_v;
+  s.moved = moved;
+  s.local_only = local_only ? 1 : 0;
+  s.R = dims->num_reqs;
+  s.Hkv = dims->num_kv_heads;
+  s.B = dims->block_size;
+  s.NBmax = dims->max_blocks;
+  s.k = k;
+  s.step = step;
+  s.copy_local = copy_local;
+  s.fetch_cap = fetch_cap < k ? fetch_cap : k;
+  *a = s;
+  return OASIS_OK;
+}
+
+oasis_status make_attn_args(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens, const uint16_t* pool_k,
+                            const uint16_t* pool_v, const int32_t* slot_map, int32_t k_slots, const int32_t* ctx_len,
+                            float scale, uint16_t* out, float* lse, void* workspace, size_t workspace_bytes,
+                            AttnArgs* a, const char* fn) {
+  oasis_status st = check_dims(dims, fn);
+  if (st != OASIS_OK) return st;
+  if (num_q_tokens < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: num_q_tokens < 1", fn);
+  if (k_slots < 0) return fail(OASIS_ERR_INVALID_ARG, "%s: k_slots < 0", fn);
+  if (!std::isfinite(scale)) return fail(OASIS_ERR_INVALID_ARG, "%s: scale is not finite", fn);
+  const int G = dims->num_q_heads / dims->num_kv_heads;
+  if ((long long)G * num_q_tokens > 80)
+    return fail(OASIS_ERR_UNSUPPORTED, "%s: G * num_q_tokens = %lld rows per KV head (at most 80)", fn,
+                (long long)G * num_q_tokens);
+  if (dims->num_reqs == 0) return OASIS_OK;
+  REQUIRE_PTR(q, fn);
+  REQUIRE_PTR(pool_k, fn);
+  REQUIRE_PTR(pool_v, fn);
+  REQUIRE_PTR(ctx_len, fn);
+  REQUIRE_PTR(out, fn);
+  if (k_slots > 0) REQUIRE_PTR(slot_map, fn);
+  const AttnPlan p = attn_plan(dims->num_reqs, dims->num_q_heads, dims->num_kv_heads, num_q_tokens,
+                               dims->block_size, k_slots);
+  if (!workspace || workspace_bytes < p.bytes)
+    return fail(OASIS_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, workspace_bytes, p.bytes);
+  AttnArgs t{};
+  t.q = q;
+  t.pool_k = pool_k;
+  t.pool_v = pool_v;
+  t.slot_map = slot_map;
+  t.ctx_len = ctx_len;
+  t.out = out;
+  t.lse = lse;
+  t.part_o = static_cast<float*>(workspace);
+  t.part_ml = static_cast<float*>(workspace) + p.part_o_floats;
+  t.R = dims->num_reqs;
+  t.Hq = dims->num_q_heads;
+  t.Hkv = dims->num_kv_heads;
+  t.G = G;
+  t.T = num_q_tokens;
+  t.B = dims->block_size;
+  t.NBmax = dims->max_blocks;
+  t.k_slots = k_slots;
+  t.scale_log2 = scale * 1.4426950408889634f;
+  t.rows = p.rows;
+  t.n_units = p.n_units;
+  t.nsplit = p.nsplit;
+  t.units_per_split = p.units_per_split;
+  *a = t;
+  return OASIS_OK;
+}
+
+}  // namespace oasis
+
+using oasis::fail;
+using oasis::hip_status;
+using oasis::ok;
+
+extern "C" {
+
+const char* oasis_last_error(void) { return oasis::last_error(); }
+
+int32_t oasis_abi_version(void) { return OASIS_ABI_VERSION; }
+
+oasis_status oasis_build_summaries(const oasis_dims* dims, const uint16_t* k_pages, int64_t num_pages,
+                                   const int32_t* block_table, const int32_t* ctx_len, uint16_t* kmax,
+                                   uint16_t* kmin, void* stream) {
+  static const char* fn = "oasis_build_summaries";
+  oasis_status st = oasis::check_dims(dims, fn);
+  if (st != OASIS_OK) return st;
+  if (dims->num_reqs == 0) return ok();
+  REQUIRE_PTR(k_pages, fn);
+  REQUIRE_PTR(block_table, fn);
+  REQUIRE_PTR(ctx_len, fn);
+  REQUIRE_PTR(kmax, fn);
+  REQUIRE_PTR(kmin, fn);
+  if (num_pages < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: num_pages < 1", fn);
+  const void* kp = nullptr;
+  st = oasis::device_view(k_pages, &kp, "k_pages", fn);
+  if (st != OASIS_OK) return st;
+  oasis::SummaryArgs a{static_cast<const uint16_t*>(kp), num_pages, block_table, ctx_len, kmax, kmin,
+                       dims->num_reqs, dims->num_kv_heads, dims->block_size, dims->max_blocks};
+  return hip_status(oasis::launch_summaries(a, static_cast<hipStream_t>(stream)), fn);
+}
+
+oasis_status oasis_score_blocks(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens,
+                                int32_t first_draft, int32_t num_draft, const uint16_t* kmax,
+                                const uint16_t* kmin, const int32_t* ctx_len, float* scores, void* stream) {
+  static const char* fn = "oasis_score_blocks";
+  oasis::ScoreArgs a{};
+  const oasis_status st =
+      oasis::make_score_args(dims, q, num_q_tokens, first_draft, num_draft, kmax, kmin, ctx_len, scores, &a, fn);
+  if (st != OASIS_OK) return st;
+  if (dims->num_reqs == 0) return ok();
+  return hip_status(oasis::launch_score(a, static_cast<hipStream_t>(stream)), fn);
+}
+
+oasis_status oasis_select_topk(const oasis_dims* dims, const float* scores, const int32_t* ctx_len, int32_t k,
+                               int32_t* sel, int32_t* sel_count, void* stream) {
+  static const char* fn = "oasis_select_topk";
+  oasis::TopkArgs a{};
+  const oasis_status st = oasis::make_topk_args(dims, scores, ctx_len, k, sel, sel_count, &a, fn);
+  if (st != OASIS_OK) return st;
+  if (dims->num_reqs == 0) return ok();
+  return hip_status(oasis::launch_topk(a, static_cast<hipStream_t>(stream)), fn);
+}
+
+oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, const uint16_t* host_v,
+                                int64_t num_pages, const int32_t* host_block_table, const int32_t* ctx_len,
+                                const int32_t* sel, const int32_t* sel_count, const float* scores, int32_t k,
+                                int32_t* slot_map, int32_t* slot_stamp, int32_t step, int32_t fetch_cap,
+                                int32_t copy_local, uint16_t* pool_k, uint16_t* pool_v, int32_t* moved,
+                                void* stream) {
+  static const char* fn = "oasis_stage_blocks";
   oasis::StageArgs a{};
+  // the host tier's device-visible addresses are resolved after every cheap check
+  oasis_status st = oasis::make_stage_args(dims, host_k, host_v, num_pages, host_block_table, ctx_len, sel,
+                                           sel_count, scores, k, slot_map, slot_stamp, step, fetch_cap, copy_local,
+                                           pool_k, pool_v, moved, &a, fn);
+  if (st != OASIS_OK) return st;
+  if (dims->num_reqs == 0) return ok();
+  const void *hk = nullptr, *hv = nullptr;
+  if ((st = oasis::device_view(host_k, &hk, "host_k", fn)) != OASIS_OK) return st;
+  if ((st = oasis::device_view(host_v, &hv, "host_v", fn)) != OASIS_OK) return st;
   a.host_k = static_cast<const uint16_t*>(hk);
   a.host_v = static_cast<const uint16_t*>(hv);
-  a.num_pages = num_pages;
-  a.block_table = host_block_table;
-  a.ctx_len = ctx_len;
-  a.sel = sel;
-  a.sel_count = sel_count;
-  a.scores = scores;
-  a.slot_map = slot_map;
-  a.slot_stamp = slot_stamp;
-  a.pool_k = pool_k;
-  a.pool_v = pool_v;
-  a.moved = moved;
-  a.local_only = local_only ? 1 : 0;
-  a.R = dims->num_reqs;
-  a.Hkv = dims->num_kv_heads;
-  a.B = dims->block_size;
-  a.NBmax = dims->max_blocks;
-  a.k = k;
-  a.step = step;
-  a.copy_local = copy_local;
-  a.fetch_cap = fetch_cap < k ? fetch_cap : k;
   return hip_status(oasis::launch_stage(a, static_cast<hipStream_t>(stream)), fn);
 }
 
 size_t oasis_attn_workspace_bytes(const oasis_dims* dims, int32_t num_q_tokens, int32_t k_slots) {
-  if (check_dims(dims, "oasis_attn_workspace_bytes") != OASIS_OK || num_q_tokens < 1 || k_slots < 0) return 0;
+  if (oasis::check_dims(dims, "oasis_attn_workspace_bytes") != OASIS_OK || num_q_tokens < 1 || k_slots < 0)
+    return 0;
   return oasis::attn_plan(dims->num_reqs, dims->num_q_heads, dims->num_kv_heads, num_q_tokens, dims->block_size,
                           k_slots)
       .bytes;
@@ -212,49 +316,11 @@ oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const uint16_t* q,
                                       int32_t k_slots, const int32_t* ctx_len, float scale, uint16_t* out,
                                       float* lse, void* workspace, size_t workspace_bytes, void* stream) {
   static const char* fn = "oasis_sparse_decode_attn";
-  oasis_status st = check_dims(dims, fn);
-  if (st != OASIS_OK) return st;
-  if (num_q_tokens < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: num_q_tokens < 1", fn);
-  if (k_slots < 0) return fail(OASIS_ERR_INVALID_ARG, "%s: k_slots < 0", fn);
-  if (!std::isfinite(scale)) return fail(OASIS_ERR_INVALID_ARG, "%s: scale is not finite", fn);
-  const int G = dims->num_q_heads / dims->num_kv_heads;
-  if ((long long)G * num_q_tokens > 80)
-    return fail(OASIS_ERR_UNSUPPORTED, "%s: G * num_q_tokens = %lld rows per KV head (at most 80)", fn,
-                (long long)G * num_q_tokens);
-  if (dims->num_reqs == 0) return ok();
-  REQUIRE_PTR(q, fn);
-  REQUIRE_PTR(pool_k, fn);
-  REQUIRE_PTR(pool_v, fn);
-  REQUIRE_PTR(ctx_len, fn);
-  REQUIRE_PTR(out, fn);
-  if (k_slots > 0) REQUIRE_PTR(slot_map, fn);
-  const oasis::AttnPlan p = oasis::attn_plan(dims->num_reqs, dims->num_q_heads, dims->num_kv_heads, num_q_tokens,
-                                             dims->block_size, k_slots);
-  if (!workspace || workspace_bytes < p.bytes)
-    return fail(OASIS_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, workspace_bytes, p.bytes);
   oasis::AttnArgs a{};
-  a.q = q;
-  a.pool_k = pool_k;
-  a.pool_v = pool_v;
-  a.slot_map = slot_map;
-  a.ctx_len = ctx_len;
-  a.out = out;
-  a.lse = lse;
-  a.part_o = static_cast<float*>(workspace);
-  a.part_ml = static_cast<float*>(workspace) + p.part_o_floats;
-  a.R = dims->num_reqs;
-  a.Hq = dims->num_q_heads;
-  a.Hkv = dims->num_kv_heads;
-  a.G = G;
-  a.T = num_q_tokens;
-  a.B = dims->block_size;
-  a.NBmax = dims->max_blocks;
-  a.k_slots = k_slots;
-  a.scale_log2 = scale * 1.4426950408889634f;
-  a.rows = p.rows;
-  a.n_units = p.n_units;
-  a.nsplit = p.nsplit;
-  a.units_per_split = p.units_per_split;
+  const oasis_status st = oasis::make_attn_args(dims, q, num_q_tokens, pool_k, pool_v, slot_map, k_slots, ctx_len,
+                                                scale, out, lse, workspace, workspace_bytes, &a, fn);
+  if (st != OASIS_OK) return st;
+  if (dims->num_reqs == 0) return ok();
   return hip_status(oasis::launch_attn(a, static_cast<hipStream_t>(stream)), fn);
 }
 

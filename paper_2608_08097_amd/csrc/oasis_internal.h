@@ -117,4 +117,33 @@ struct AttnPlan {
 AttnPlan attn_plan(int R, int Hq, int Hkv, int T, int B, int k_slots);
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
 
+// --- argument checks shared by the entry points (api.hip) ---------------------
+// Each builder validates like the entry point of the same operation (fn names
+// it in the message) and fills the kernel arguments; with num_reqs == 0 it
+// returns OASIS_OK without checking pointers and leaves *a untouched.
+
+oasis_status fail(oasis_status st, const char* fmt, ...);
+oasis_status ok();
+const char* last_error();
+oasis_status hip_status(hipError_t e, const char* where);
+oasis_status check_dims(const oasis_dims* d, const char* fn);
+// Device-visible address of pinned host memory (or of device memory as is).
+oasis_status device_view(const void* p, const void** out, const char* what, const char* fn);
+
+oasis_status make_score_args(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens, int32_t first_draft,
+                             int32_t num_draft, const uint16_t* kmax, const uint16_t* kmin, const int32_t* ctx_len,
+                             float* scores, ScoreArgs* a, const char* fn);
+oasis_status make_topk_args(const oasis_dims* dims, const float* scores, const int32_t* ctx_len, int32_t k,
+                            int32_t* sel, int32_t* sel_count, TopkArgs* a, const char* fn);
+oasis_status make_stage_args(const oasis_dims* dims, const uint16_t* host_k, const uint16_t* host_v,
+                             int64_t num_pages, const int32_t* host_block_table, const int32_t* ctx_len,
+                             const int32_t* sel, const int32_t* sel_count, const float* scores, int32_t k,
+                             int32_t* slot_map, int32_t* slot_stamp, int32_t step, int32_t fetch_cap,
+                             int32_t copy_local, uint16_t* pool_k, uint16_t* pool_v, int32_t* moved, StageArgs* a,
+                             const char* fn);
+oasis_status make_attn_args(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens, const uint16_t* pool_k,
+                            const uint16_t* pool_v, const int32_t* slot_map, int32_t k_slots, const int32_t* ctx_len,
+                            float scale, uint16_t* out, float* lse, void* workspace, size_t workspace_bytes,
+                            AttnArgs* a, const char* fn);
+
 }  // namespace oasis

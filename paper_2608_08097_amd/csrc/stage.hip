@@ -10,22 +10,26 @@
 // the selected block-head entries from pinned host memory over PCIe and
 // writes them into the resident GPU pages.
 //
-// A small fixed grid of 256-thread workgroups walks the (request, KV head)
-// pairs (workgroup w takes pairs w, w + grid, ...); for each pair it does:
-//   plan   the slot map, stamps and selection sit in LDS; ranks come from
-//          workgroup scans (free slots, misses) and from counting (stale
-//          slots by (stamp, slot)); slot_map / slot_stamp are updated in place
-//          and the (slot, page) pairs stay in LDS;
+// A fixed grid of up to kCopyWorkgroups 256-thread workgroups walks the
+// (request, KV head) pairs (workgroup w takes pairs w, w + grid, ...); for each
+// pair it does:
+//   plan   the slot map, stamps and selection sit in LDS; misses and stale
+//          slots are compacted by workgroup scans and ranked one item per
+//          thread (misses by score under a cap, stale slots by (stamp, slot));
+//          slot_map / slot_stamp are updated in place and the (slot, page)
+//          pairs stay in LDS;
 //   copy   the entries are streamed in batches of PF: the PCIe loads of a
 //          whole batch (PF x 2 x B x d x 2 bytes) are issued before any is
 //          stored, K goes to the pool token-major, V is transposed through LDS
 //          into the d x B layout the attention kernel reads.
-// Host reads wait microseconds in the memory system, and while they are
-// outstanding they slow the HBM traffic of every concurrent kernel (measured
-// on MI355X: 64 copying workgroups triple the duration of a concurrent block
-// scan, 16 add about 20 %, and 16 x 8 KiB in flight already saturate the
-// link). So the grid holds at most kCopyWorkgroups workgroups with about
-// kCopyInflight entries in flight between them.
+// Host reads take microseconds to return, so the plans run one pair per
+// workgroup in parallel and each workgroup keeps a batch of entries in flight.
+// Host reads beyond what saturates the link only queue inside the GPU, where
+// they slow the HBM traffic of concurrent kernels: measured on MI355X with a
+// capped delta of 3 MB per step, 8 entries per workgroup in flight (3 MB)
+// stretch a concurrent block scan from 57 to 98 us, 2 entries (2 MB) to 88 us
+// at the same transfer time, and 1 entry on 32 workgroups to 77 us but with a
+// transfer 20 % slower; 64 workgroups x 2 entries gave the best step rate.
 #include <climits>
 
 #include "oasis_internal.h"
@@ -37,8 +41,9 @@ namespace {
 constexpr int kPlanThreads = 256;
 constexpr int kMaxK = 1024;
 constexpr int kPer = kMaxK / kPlanThreads;  // items per thread in the scans
-constexpr int kCopyWorkgroups = 32;
-constexpr int kCopyInflight = 32;  // block-head entries (K and V) in flight over the whole grid
+constexpr int kKeyPad = 4;
+constexpr int kCopyWorkgroups = 64;
+constexpr int kCopyInflight = 128;  // block-head entries (K and V) in flight over the whole grid
 
 // Monotone map of a float onto uint32 (larger float, larger key; -0 and +0 equal).
 __device__ inline unsigned order_key(float f) {
@@ -69,11 +74,20 @@ __device__ int wg_exclusive_scan(int v, int* s_wave) {
 }
 
 // Plan of one (request, KV head); returns the number of entries in s_slot/s_page.
+//
+// Misses and stale slots are first compacted (in ascending selection index and
+// ascending slot, which is ascending block id and slot order); each thread then
+// ranks one compacted item against all others, reading the keys four at a time
+// from LDS, so no thread walks a long chain of dependent reads.
 __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int* s_page, int* s_wave) {
   const int tid = threadIdx.x;
   const int k = a.k;
-  __shared__ int s_sel[kMaxK], s_map[kMaxK], s_stamp[kMaxK], s_hit[kMaxK], s_keep[kMaxK], s_vict[kMaxK];
-  __shared__ unsigned s_key[kMaxK];
+  // by selection index: s_sel, s_hit; by slot: s_map, s_stamp, s_keep; victims in order: s_vict;
+  // compacted misses: key, selection index, admitted; compacted stale slots: stamp, slot
+  __shared__ int s_sel[kMaxK], s_hit[kMaxK], s_map[kMaxK], s_stamp[kMaxK], s_keep[kMaxK], s_vict[kMaxK];
+  __shared__ __align__(16) unsigned s_mkey[kMaxK + kKeyPad];
+  __shared__ __align__(16) int s_skey[kMaxK + kKeyPad];
+  __shared__ int s_midx[kMaxK], s_madm[kMaxK], s_sslot[kMaxK];
 
   const long long base = (long long)rh * k;
   int m = a.sel_count[rh];
@@ -83,7 +97,6 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
     s_hit[i] = 0;
     s_map[i] = a.slot_map[base + i];
     s_stamp[i] = a.slot_stamp[base + i];
-    s_vict[i] = -1;
   }
   __syncthreads();
 
@@ -106,102 +119,125 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
   }
   __syncthreads();
 
-  // items [tid*kPer, tid*kPer + kPer): misses (selection order) and free slots (slot order)
+  // items [i0, i0 + kPer): selection entries (misses) and slots (free, stale)
   const int i0 = tid * kPer;
-  int n_miss_local = 0, n_free_local = 0;
+  int nm = 0, nf = 0, ns = 0;
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     const int i = i0 + j;
-    if (i < m && !s_hit[i]) ++n_miss_local;
-    if (i < k && s_map[i] < 0) ++n_free_local;
+    if (i < m && !s_hit[i]) ++nm;
+    if (i < k) {
+      if (s_map[i] < 0) ++nf;
+      else if (!s_keep[i]) ++ns;
+    }
   }
-  wg_exclusive_scan(n_miss_local, s_wave);
-  const int n_miss = s_wave[4];
-  const int free_base = wg_exclusive_scan(n_free_local, s_wave);
-  const int n_free = s_wave[4];
+  const int mf_base = wg_exclusive_scan(nm | (nf << 16), s_wave);  // two 16-bit counts (<= 1024 each)
+  const int mf_tot = s_wave[4];
+  const int st_base = wg_exclusive_scan(ns, s_wave);
+  const int n_stale = s_wave[4];
+  const int n_miss = mf_tot & 0xFFFF;
+  const int n_free = mf_tot >> 16;
 
   // admission: every miss, or under a binding cap the fetch_cap misses with the
-  // highest score (ties: lowest block id, i.e. lowest selection index). Keys are
-  // order-preserving integers, so the ranks are distinct even for NaN scores and
-  // exactly fetch_cap misses are admitted.
+  // highest score (ties: lowest block id). Keys are order-preserving integers, so
+  // the ranks are distinct even for NaN scores and exactly fetch_cap misses are
+  // admitted.
   const bool capped = a.fetch_cap < n_miss;
-  if (capped) {
-    for (int i = tid; i < m; i += kPlanThreads) {
-      const int b = s_sel[i];
-      const float sc = (b >= 0 && b < a.NBmax) ? a.scores[(long long)rh * a.NBmax + b] : -__builtin_inff();
-      s_key[i] = s_hit[i] ? 0u : order_key(sc);
-    }
-    __syncthreads();
-  }
-  unsigned adm_bits = 0;
-  int n_adm_local = 0;
-#pragma unroll
-  for (int j = 0; j < kPer; ++j) {
-    const int i = i0 + j;
-    if (i >= m || s_hit[i]) continue;
-    bool adm = true;
-    if (capped) {
-      const unsigned key = s_key[i];
-      int rank = 0;
-      for (int t = 0; t < m; ++t) {
-        if (s_hit[t]) continue;
-        const unsigned kt = s_key[t];
-        rank += (kt > key) || (kt == key && t < i);
-      }
-      adm = rank < a.fetch_cap;
-    }
-    if (adm) {
-      adm_bits |= 1u << j;
-      ++n_adm_local;
-    }
-  }
-  const int adm_base = wg_exclusive_scan(n_adm_local, s_wave);
-  const int n_adm = s_wave[4];
-
-  // victim order: free slots ascending, then stale residents by (stamp, slot)
   {
-    int fr = free_base;
-#pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      const int s = i0 + j;
-      if (s < k && s_map[s] < 0) s_vict[fr++] = s;
-    }
-  }
-  for (int s = tid; s < k; s += kPlanThreads) {
-    if (s_map[s] < 0 || s_keep[s]) continue;
-    const int st = s_stamp[s];
-    int rank = n_free;
-    for (int t = 0; t < k; ++t) {
-      if (s_map[t] < 0 || s_keep[t]) continue;
-      const int su = s_stamp[t];
-      rank += (su < st) || (su == st && t < s);
-    }
-    s_vict[rank] = s;
-  }
-  __syncthreads();
-
-  // pair the i-th admitted miss (ascending block id) with the i-th victim
-  int moved_local = 0;
-  {
-    int mr = adm_base;
+    int mr = mf_base & 0xFFFF, fr = mf_base >> 16, sr = st_base;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int i = i0 + j;
-      if (!(adm_bits >> j & 1u)) continue;
+      if (i < m && !s_hit[i]) {
+        unsigned key = 0;
+        if (capped) {
+          const int b = s_sel[i];
+          key = order_key((b >= 0 && b < a.NBmax) ? a.scores[(long long)rh * a.NBmax + b] : -__builtin_inff());
+        }
+        s_mkey[mr] = key;
+        s_midx[mr] = i;
+        ++mr;
+      }
+      if (i < k) {
+        if (s_map[i] < 0) {
+          s_vict[fr++] = i;
+        } else if (!s_keep[i]) {
+          s_skey[sr] = s_stamp[i];
+          s_sslot[sr] = i;
+          ++sr;
+        }
+      }
+    }
+    // pads read by the 4-wide loops below; they never rank ahead of a real item
+    if (tid < kKeyPad) {
+      s_mkey[n_miss + tid] = 0u;
+      s_skey[n_stale + tid] = INT_MAX;
+    }
+  }
+  __syncthreads();
+
+  for (int c = tid; c < n_miss; c += kPlanThreads) {
+    int adm = 1;
+    if (capped) {
+      const unsigned key = s_mkey[c];
+      int rank = 0;
+#pragma unroll 4
+      for (int t = 0; t < n_miss; t += 4) {
+        const u32x4 kt = *reinterpret_cast<const u32x4*>(&s_mkey[t]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) rank += (kt[e] > key) || (kt[e] == key && t + e < c);
+      }
+      adm = rank < a.fetch_cap;
+    }
+    s_madm[c] = adm;
+  }
+  // victim order: free slots ascending (already in s_vict), then stale slots by (stamp, slot)
+  for (int c = tid; c < n_stale; c += kPlanThreads) {
+    const int st = s_skey[c];
+    int rank = 0;
+#pragma unroll 4
+    for (int t = 0; t < n_stale; t += 4) {
+      const int4 kt = *reinterpret_cast<const int4*>(&s_skey[t]);
+      rank += (kt.x < st) || (kt.x == st && t < c);
+      rank += (kt.y < st) || (kt.y == st && t + 1 < c);
+      rank += (kt.z < st) || (kt.z == st && t + 2 < c);
+      rank += (kt.w < st) || (kt.w == st && t + 3 < c);
+    }
+    s_vict[n_free + rank] = s_sslot[c];
+  }
+  __syncthreads();
+
+  // the i-th admitted miss (ascending block id) goes to the i-th victim
+  int na = 0;
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int c = i0 + j;
+    if (c < n_miss && s_madm[c]) ++na;
+  }
+  const int adm_base = wg_exclusive_scan(na, s_wave);
+  const int n_adm = s_wave[4];
+  const int n_vict = n_free + n_stale;
+  int moved_local = 0;
+  {
+    int ar = adm_base;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int c = i0 + j;
+      if (c >= n_miss || !s_madm[c]) continue;
       // a slot map holding one block twice can leave fewer victims than misses
-      const int v = mr < k ? s_vict[mr] : -1;
-      const int blk = s_sel[i];
+      const int v = ar < n_vict ? s_vict[ar] : -1;
+      const int blk = s_sel[s_midx[c]];
       int page = -1;
       if (v >= 0 && blk >= 0 && blk < a.NBmax) page = a.block_table[(long long)r * a.NBmax + blk];
       if (page < 0 || page >= a.num_pages) page = -1;
-      s_slot[mr] = v;
-      s_page[mr] = page;
+      s_slot[ar] = v;
+      s_page[ar] = page;
       if (v >= 0) {
         s_map[v] = page >= 0 ? blk : -1;
         s_keep[v] = page >= 0;
       }
       moved_local += page >= 0;
-      ++mr;
+      ++ar;
     }
   }
   wg_exclusive_scan(moved_local, s_wave);

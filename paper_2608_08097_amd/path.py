@@ -43,6 +43,8 @@ class LayerState:
                                    device=dev)
         self.ev_staged = None   # recorded after the last stage of this layer
         self.ev_attended = None  # recorded after the last attention of this layer
+        self.layer_id = None    # id in the native issuer of the DecodePath that runs it
+        self.pipe = None
 
     def reset(self):
         self.slot_map.fill_(-1)
@@ -88,8 +90,14 @@ class DecodePath:
 
     def __init__(self, d: L.OasisDims, num_q_tokens: int, k: int, host_k: torch.Tensor, host_v: torch.Tensor,
                  block_table: torch.Tensor, first_draft: int = 1, num_draft: int | None = None,
-                 scale: float | None = None, fetch_cap: int | None = None):
+                 scale: float | None = None, fetch_cap: int | None = None, native: bool = True,
+                 max_layers: int = 256):
         self.dims, self.T, self.k = d, int(num_q_tokens), int(k)
+        # step_pipelined issues through the library's native step issuer unless a timer is given
+        self.native = bool(native)
+        self.max_layers = int(max_layers)
+        self._pipe = None
+        self._n_layers = 0
         # admitted misses per (request, KV head) and step; k admits every miss
         self.fetch_cap = self.k if fetch_cap is None else int(fetch_cap)
         self.first_draft = int(first_draft)
@@ -102,6 +110,48 @@ class DecodePath:
 
     def new_layer(self) -> LayerState:
         return LayerState(self.dims, self.T, self.k, self.block_table.device)
+
+    def _native_layer(self, st: LayerState) -> int:
+        """Handle of the native issuer and the layer id of ``st`` (registered on first use)."""
+        if self._pipe is None:
+            self._pipe = L.oasis_pipeline_create(self.dims, self.T, self.first_draft, self.num_draft, self.k,
+                                                 self.fetch_cap, self.scale, self.host_k, self.host_v,
+                                                 self.block_table, self.max_layers, self.side, self.xfer)
+        lid = getattr(st, "layer_id", None)
+        if lid is None or getattr(st, "pipe", None) != self._pipe:
+            if self._n_layers >= self.max_layers:
+                raise RuntimeError(f"more than {self.max_layers} layers on one DecodePath")
+            lid = self._n_layers
+            self._n_layers += 1
+            L.oasis_pipeline_set_layer(self._pipe, lid, self.dims, self.T, self.k, st.kmax, st.kmin, st.scores,
+                                       st.sel, st.sel_count, st.slot_map, st.slot_stamp, st.pool_k, st.pool_v,
+                                       st.moved, st.out, st.lse, st.ws_attn)
+            st.layer_id, st.pipe = lid, self._pipe
+        return lid
+
+    def profile_begin(self, max_steps: int):
+        """Time every kernel of the next ``max_steps`` native steps on its own stream."""
+        if self._pipe is None:
+            raise RuntimeError("no native step has been issued yet")
+        L.oasis_pipeline_profile_begin(self._pipe, max_steps)
+
+    def profile_end(self) -> tuple[dict[str, float], int]:
+        """Mean durations (us) of attention, scoring, top-K and staging, and the step count."""
+        return L.oasis_pipeline_profile_end(self._pipe)
+
+    def close(self):
+        """Wait for the background streams and release the native issuer."""
+        if self._pipe is not None:
+            self.side.synchronize()
+            self.xfer.synchronize()
+            L.oasis_pipeline_destroy(self._pipe)
+            self._pipe = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
     # -- individual steps (all asynchronous on `stream`) ----------------------
     def build_summaries(self, st: LayerState, ctx_len: torch.Tensor, k_pages: torch.Tensor | None = None,
@@ -154,7 +204,15 @@ class DecodePath:
         every step; otherwise the transfer refreshes it.
         ``timer`` records HIP events around each call on its own stream;
         ``moved`` (int32 [R][Hkv]) receives the entries this step copies.
+        Without a timer the step goes through the library's native issuer (one
+        C call); with one it is issued call by call from here. Switching between
+        the two for one layer needs a device synchronization in between.
         """
+        if timer is None and self.native:
+            lid = self._native_layer(st)
+            L.oasis_pipeline_step(self._pipe, lid, q, ctx_len, step, growing, moved,
+                                  torch.cuda.current_stream())
+            return
         tm = timer if timer is not None else _NO_TIMER
         fg = torch.cuda.current_stream()
         pred, xfer = self.side, self.xfer

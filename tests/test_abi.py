@@ -83,6 +83,29 @@ def test_argument_checks_without_gpu(lib):
     assert lib.oasis_last_error() == ""
 
 
+def test_pipeline_argument_checks_without_gpu(lib):
+    L = lib.lib()
+    h = ctypes.c_void_p(123)
+    d = lib.dims(1, 32, 8, 128, 16, 512)
+    assert L.oasis_pipeline_create(ctypes.byref(d), 5, 1, 4, 128, 6, 1.0, None, None, 10, None, 8, None, None,
+                                   None) == 1
+    bad = lib.dims(1, 32, 8, 64, 16, 512)
+    assert L.oasis_pipeline_create(ctypes.byref(bad), 5, 1, 4, 128, 6, 1.0, None, None, 10, None, 8, None, None,
+                                   ctypes.byref(h)) == 2
+    assert h.value is None                      # cleared on failure
+    assert L.oasis_pipeline_create(ctypes.byref(d), 5, 1, 4, 128, 6, 1.0, None, None, 10, None, 0, None, None,
+                                   ctypes.byref(h)) == 1
+    assert "max_layers" in lib.oasis_last_error()
+    assert L.oasis_pipeline_create(ctypes.byref(d), 5, 1, 4, 128, 6, 1.0, None, None, 10, None, 8, 1, None,
+                                   ctypes.byref(h)) == 1
+    assert L.oasis_pipeline_set_layer(None, 0, None) == 1
+    assert L.oasis_pipeline_step(None, 0, None, None, 0, 0, None, None) == 1
+    assert L.oasis_pipeline_join(None, None) == 1
+    assert L.oasis_pipeline_profile_begin(None, 4) == 1
+    assert L.oasis_pipeline_profile_end(None, None, None) == 1
+    L.oasis_pipeline_destroy(None)
+
+
 def test_workspace_sizes(lib):
     d = lib.dims(8, 32, 8, 128, 16, 8192)
     ws = lib.oasis_attn_workspace_bytes(d, 5, 128)

@@ -344,8 +344,9 @@ def test_dense_equivalence():
     assert_lse_close(st.lse.cpu().numpy(), ref_l)
 
 
+@pytest.mark.parametrize("issue", ["native", "python"])
 @pytest.mark.parametrize("cap", [None, 2])
-def test_pipelined_multistep(cap):
+def test_pipelined_multistep(cap, issue):
     """Reasoning-style loop: AR(1) queries, one token per step, attention on the previous step's staging.
 
     With a fetch cap, later steps attend stale residents in place of the misses
@@ -358,7 +359,7 @@ def test_pipelined_multistep(cap):
     hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
     d = _dims(w)
     k = c.K
-    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap)
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap, native=issue == "native")
     st = LayerState(d, c.T, k)
     smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
     stamp = np.zeros_like(smap)
@@ -377,7 +378,7 @@ def test_pipelined_multistep(cap):
         sel, cnt = O.select_topk(sc, ctx, k, c.block_size)
         moved = O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, s, pk, pv, ctx, c.block_size,
                                copy_local=False, scores=sc, fetch_cap=cap)
-        note(f"pipelined step {s} cap={cap}")
+        note(f"pipelined step {s} cap={cap} issue={issue}")
         ctx_d, q_d = dev_i32(ctx), dev_bf16(q)
         path.build_summaries(st, ctx_d)   # summaries of blocks completed so far
         path.step_pipelined(st, q_d, ctx_d, s, growing=True)
@@ -393,6 +394,125 @@ def test_pipelined_multistep(cap):
             assert moved.sum() < cnt.sum(), "AR(1) drift: later steps are deltas"
         if cap is not None:
             assert moved.max() <= cap
+
+
+def test_pipelined_layers_native():
+    """Several layers interleaved on the native issuer with no host synchronization
+    between steps (paper §4.2.2: per-layer chains, layer-local waits); every
+    layer's final state equals its own oracle chain."""
+    n_layers, rounds, cap = 3, 4, 3
+    w = make_workload("c2", num_reqs=3, ctx_args=(900, 2500), budget=16 * 20, ar_queries=True)
+    c = w.cfg
+    hk_t, hv_t = pinned_pages(w)
+    hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
+    d = _dims(w)
+    k = c.K
+    ctx = w.ctx_len(0)
+    ctx_d = dev_i32(ctx)
+    qs = [w.layer_queries(l, rounds + 1) for l in range(n_layers)]
+    kmax, kmin = O.block_summaries(hk, w.block_table, ctx, c.block_size, w.NBmax)
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap)
+    layers = [LayerState(d, c.T, k) for _ in range(n_layers)]
+    ref = []
+    for l, st in enumerate(layers):
+        # initial working set: one uncapped fill from the layer's first prediction
+        path.build_summaries(st, ctx_d)
+        path.predict(st, dev_bf16(qs[l][0]), ctx_d)
+        path.stage(st, ctx_d, 0, fetch_cap=k)
+        smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
+        stamp = np.zeros_like(smap)
+        pk = np.zeros((c.num_reqs, k + 1, c.num_kv_heads, c.block_size, c.head_dim), np.uint16)
+        pv = np.zeros_like(pk)
+        sc = O.block_scores(qs[l][0], kmax, kmin, ctx, c.num_kv_heads, c.block_size)
+        sel, cnt = O.select_topk(sc, ctx, k, c.block_size)
+        O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, 0, pk, pv, ctx, c.block_size)
+        ref.append(dict(smap=smap, stamp=stamp, pk=pk, pv=pv))
+    q_dev = [[dev_bf16(x) for x in qs[l]] for l in range(n_layers)]
+    note("native pipelined layers: issuing")
+    for s in range(1, rounds + 1):
+        for l in range(n_layers):
+            path.step_pipelined(layers[l], q_dev[l][s], ctx_d, s)
+    path.join()
+    torch.cuda.synchronize()
+    for l in range(n_layers):
+        r = ref[l]
+        for s in range(1, rounds + 1):
+            q = qs[l][s]
+            ref_o, ref_l = O.sparse_attend(q, r["pk"], r["pv"], r["smap"], ctx, c.block_size)
+            sc = O.block_scores(q, kmax, kmin, ctx, c.num_kv_heads, c.block_size)
+            sel, cnt = O.select_topk(sc, ctx, k, c.block_size)
+            O.stage_blocks(hk, hv, w.block_table, sel, cnt, r["smap"], r["stamp"], s, r["pk"], r["pv"], ctx,
+                           c.block_size, scores=sc, fetch_cap=cap)
+        st = layers[l]
+        assert_attn_close(host_bits(st.out), ref_o, f"layer {l} out")
+        assert_lse_close(st.lse.cpu().numpy(), ref_l)
+        assert np.array_equal(st.slot_map.cpu().numpy(), r["smap"]), l
+        assert np.array_equal(st.slot_stamp.cpu().numpy(), r["stamp"]), l
+        assert np.array_equal(host_bits(st.pool_k), r["pk"]), l
+        assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), r["pv"]), l
+    path.close()
+
+
+def test_pipeline_profile():
+    """The native issuer's kernel timing records one span per kernel kind per step."""
+    w = make_workload("c2", num_reqs=2, ctx_args=(3000, 5000), budget=16 * 32, ar_queries=True)
+    c = w.cfg
+    hk_t, hv_t = pinned_pages(w)
+    d = _dims(w)
+    ctx_d = dev_i32(w.ctx_len(0))
+    qs = [dev_bf16(x) for x in w.layer_queries(0, 5)]
+    path = DecodePath(d, c.T, c.K, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=4)
+    st = LayerState(d, c.T, c.K)
+    path.build_summaries(st, ctx_d)
+    note("pipeline profile")
+    path.step_pipelined(st, qs[0], ctx_d, 0)
+    path.profile_begin(3)
+    for s in range(1, 5):                      # one step more than profiled
+        path.step_pipelined(st, qs[s], ctx_d, s)
+    path.join()
+    torch.cuda.synchronize()
+    us, n = path.profile_end()
+    assert n == 3
+    assert all(0.0 < us[k_] < 1e5 for k_ in ("attn", "score", "topk", "stage")), us
+    with pytest.raises(P.OasisError):
+        path.profile_end()
+    path.close()
+
+
+def test_pipeline_abi_errors_on_device():
+    w = make_workload("c2", num_reqs=1, ctx_args=(500, 500), budget=16 * 8)
+    c = w.cfg
+    hk_t, hv_t = pinned_pages(w)
+    d = _dims(w)
+    bt = dev_i32(w.block_table)
+    with pytest.raises(P.OasisError) as e:      # fetch cap below 1
+        P.oasis_pipeline_create(d, c.T, 1, c.num_draft, c.K, 0, None, hk_t, hv_t, bt, 4)
+    assert e.value.status == 1
+    with pytest.raises(ValueError):             # host tier neither pinned nor on the device
+        P.oasis_pipeline_create(d, c.T, 1, c.num_draft, c.K, c.K, None, hk_t.clone(), hv_t.clone(), bt, 4)
+    h = P.oasis_pipeline_create(d, c.T, 1, c.num_draft, c.K, c.K, None, hk_t, hv_t, bt, 4)
+    try:
+        q = torch.zeros((1, c.T, c.num_q_heads, c.head_dim), dtype=torch.bfloat16, device="cuda")
+        ctx = dev_i32(w.ctx_len(0))
+        with pytest.raises(P.OasisError) as e:  # layer never registered
+            P.oasis_pipeline_step(h, 0, q, ctx, 0, False)
+        assert e.value.status == 1 and "set_layer" in str(e.value)
+        st = LayerState(d, c.T, c.K)
+        small_ws = torch.zeros(4, dtype=torch.uint8, device="cuda")
+        P.oasis_pipeline_set_layer(h, 0, d, c.T, c.K, st.kmax, st.kmin, st.scores, st.sel, st.sel_count,
+                                   st.slot_map, st.slot_stamp, st.pool_k, st.pool_v, st.moved, st.out, st.lse,
+                                   small_ws)
+        with pytest.raises(P.OasisError) as e:  # workspace too small, caught by the per-step checks
+            P.oasis_pipeline_step(h, 0, q, ctx, 0, False)
+        assert e.value.status == 4
+        with pytest.raises(P.OasisError) as e:
+            P.oasis_pipeline_set_layer(h, 4, d, c.T, c.K, st.kmax, st.kmin, st.scores, st.sel, st.sel_count,
+                                       st.slot_map, st.slot_stamp, st.pool_k, st.pool_v, st.moved, st.out,
+                                       st.lse, st.ws_attn)
+        assert e.value.status == 1
+    finally:
+        torch.cuda.synchronize()
+        P.oasis_pipeline_destroy(h)
 
 
 # ---------------------------------------------------------------------------

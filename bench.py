@@ -1,12 +1,19 @@
 """Benchmark of the OasisKV decode-time hot path on one MI355X.
 
 One step = one pass of the whole path for one layer of a batch: attention of
-the stacked (verify + draft) queries over the HBM working set, and, on a
-background stream, block scoring from the draft queries, top-K selection and
-the delta staging of the selected blocks from the pinned host tier (paper
-§4.2.2 schedule for one layer). The value is decode steps per second per
-layer with every input resident in HBM (or in pinned host memory for the host
-tier) when the timed region starts.
+the stacked (verify + draft) queries over the HBM working set, and, on
+background streams, block scoring from the draft queries, top-K selection and
+the delta staging of the selected blocks from the pinned host tier under the
+fetch cap (paper §4.2.2 schedule for one layer, §5.5.1 default fetch ratio
+0.05). The value is decode steps per second per layer with every input
+resident in HBM (or in pinned host memory for the host tier) when the timed
+region starts.
+
+Timed regions: (1) the step rate, steps issued through the native step issuer
+with nothing else on the streams; (2) the same steps again with dispatch-timed
+events on every kernel (durations inside the running pipeline); (3) each
+kernel alone, back to back, for the roofline of the dominant kernel (the
+scorer) and the attention.
 
 Workload (default): long-context serving, 8 requests x 131,072 tokens, GQA
 32 query / 8 KV heads, head_dim 128, block 16 (8,192 blocks), 4 draft tokens,
@@ -41,6 +48,23 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+TRAFFIC_NOTE = os.path.join(ROOT, "profiles", "score_kernel_c4_hbm_traffic.md")
+
+
+def measured_traffic():
+    """HBM bytes per scorer launch from the committed FETCH_SIZE / WRITE_SIZE passes, or None
+    if they were taken on a different score.hip (or are missing)."""
+    import hashlib
+    import re
+    try:
+        note = open(TRAFFIC_NOTE).read()
+        src = open(os.path.join(ROOT, "paper_2608_08097_amd", "csrc", "score.hip"), "rb").read()
+    except OSError:
+        return None
+    m = re.search(r"score_kernel_traffic_bytes=(\d+) score_hip_sha256=([0-9a-f]{64})", note)
+    if not m or m.group(2) != hashlib.sha256(src).hexdigest():
+        return None
+    return int(m.group(1))
 
 
 def parse():
@@ -56,8 +80,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention comparison")
-    ap.add_argument("--isolated", action="store_true",
-                    help="also time score / top-K / attention alone (one stream, rotating layers)")
+    ap.add_argument("--kernels-only", action="store_true",
+                    help="only time the kernels alone on one stream (for hardware-counter passes)")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a plain 1 GiB device copy (for scaling FETCH_SIZE/WRITE_SIZE counters)")
     return ap.parse_args()
@@ -185,6 +209,13 @@ def main():
         path.stage(st, ctx_d, 0, fetch_cap=K)
     moved_log = torch.zeros((args.steps, c.num_reqs, c.num_kv_heads), dtype=torch.int32, device="cuda")
     torch.cuda.synchronize()
+    if args.kernels_only:
+        # For hardware-counter passes, which serialize dispatches: no cross-stream
+        # waits may be in flight, so only the single-stream region 3 runs.
+        iso = isolated(P, torch, path, layers, qs, ctx_d)
+        torch.cuda.synchronize()
+        print(json.dumps({"kernels_only": {k_: round(v, 2) for k_, v in iso.items()}}), flush=True)
+        return
 
     def run(i, timed):
         l, s = i % NL, i // NL
@@ -226,8 +257,12 @@ def main():
     entry_bytes = 2 * c.block_size * c.head_dim * 2
     moved = moved_rate
     h2d_per_step = float(moved.sum()) / args.steps * entry_bytes
-    score_gbs = score_bytes / (us["score"] * 1e3) if us["score"] > 0 else 0.0
-    attn_gbs = attn_bytes / (us["attn"] * 1e3) if us["attn"] > 0 else 0.0
+    # Timed region 3: each kernel alone, back to back on the current stream over
+    # the rotating layer states between one pair of HIP events (the per-launch
+    # event cost vanishes; this is the duration a kernel trace reports).
+    iso = isolated(P, torch, path, layers, qs, ctx_d)
+    score_gbs = score_bytes / (iso["score"] * 1e3)
+    attn_gbs = attn_bytes / (iso["attn"] * 1e3)
 
     dense = None
     if not args.no_dense and args.workload == "c4":
@@ -258,27 +293,29 @@ def main():
         "roofline": {
             "bound": "hbm", "kernel": "score_kernel (oasis_score_blocks)",
             "achieved": round(score_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(score_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-            "algorithmic_bytes": score_bytes, "avg_us": round(us["score"], 2),
+            "frac": round(score_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
+            "algorithmic_bytes": score_bytes, "avg_us": round(iso["score"], 2),
+            "timing": "64 back-to-back launches over the rotating layer states, one event pair",
         },
-        "attention": {"avg_us": round(us["attn"], 2), "algorithmic_bytes": attn_bytes,
+        "attention": {"avg_us": round(iso["attn"], 2), "algorithmic_bytes": attn_bytes,
                       "achieved_GBs": round(attn_gbs, 1), "frac": round(attn_gbs / HBM_PEAK_GBS, 4)},
-        "topk_us": round(us["topk"], 2),
-        "staging": {"avg_us": round(us["stage"], 2), "h2d_bytes_per_step": round(h2d_per_step),
+        "topk_us": round(iso["topk"], 2),
+        "staging": {"avg_us_in_pipeline": round(us["stage"], 2), "h2d_bytes_per_step": round(h2d_per_step),
                     "entries_per_step": round(float(moved.sum()) / args.steps, 1),
                     "h2d_GBs": round(h2d_per_step / (us["stage"] * 1e3), 2) if us["stage"] > 0 else None},
+        # region 2: dispatch-timed events per kernel inside the running pipeline; they include the
+        # slowdown from concurrent kernels and host reads, and a few us of event latency each
+        "pipeline_kernel_us": {k_: round(v, 2) for k_, v in us.items()},
         "dense_attention": dense,
     }
-    if args.isolated:
-        result["isolated"] = isolated(P, torch, path, layers, qs, ctx_d, score_bytes, attn_bytes)
     if not args.no_cpu_baseline:
         log("timing the oracle sample")
         result["cpu_baseline"] = cpu_baseline(w, hk, hv, w.layer_queries(0, 64), K, fetch_cap, args.cpu_seconds)
     print(json.dumps(result), flush=True)
 
 
-def isolated(P, torch, path, layers, qs, ctx_d, score_bytes, attn_bytes, iters=64):
-    """Each kernel alone on the current stream, rotating over the layer states."""
+def isolated(P, torch, path, layers, qs, ctx_d, iters=64):
+    """Mean duration (us) of each kernel alone on the current stream, rotating over the layer states."""
     d, T, K = path.dims, path.T, path.k
     NL = len(layers)
     res = {}
@@ -294,13 +331,11 @@ def isolated(P, torch, path, layers, qs, ctx_d, score_bytes, attn_bytes, iters=6
         torch.cuda.synchronize()
         return 1000.0 * e0.elapsed_time(e1) / iters
 
-    us = timeit(lambda st, q: P.oasis_score_blocks(d, q, T, 1, T - 1, st.kmax, st.kmin, ctx_d, st.scores))
-    res["score"] = {"avg_us": round(us, 2), "GBs": round(score_bytes / (us * 1e3), 1)}
-    us = timeit(lambda st, q: P.oasis_select_topk(d, st.scores, ctx_d, K, st.sel, st.sel_count))
-    res["topk"] = {"avg_us": round(us, 2)}
-    us = timeit(lambda st, q: P.oasis_sparse_decode_attn(d, q, T, st.pool_k, st.pool_v, st.slot_map, K, ctx_d,
-                                                         None, st.out, st.lse, st.ws_attn))
-    res["attn"] = {"avg_us": round(us, 2), "GBs": round(attn_bytes / (us * 1e3), 1)}
+    res["score"] = timeit(lambda st, q: P.oasis_score_blocks(d, q, T, 1, T - 1, st.kmax, st.kmin, ctx_d,
+                                                            st.scores))
+    res["topk"] = timeit(lambda st, q: P.oasis_select_topk(d, st.scores, ctx_d, K, st.sel, st.sel_count))
+    res["attn"] = timeit(lambda st, q: P.oasis_sparse_decode_attn(d, q, T, st.pool_k, st.pool_v, st.slot_map, K,
+                                                                  ctx_d, None, st.out, st.lse, st.ws_attn))
     return res
 
 

@@ -291,8 +291,9 @@ OASIS_API oasis_status oasis_pipeline_step(oasis_pipeline* pipeline, int32_t lay
 /* Make `stream` wait for all work issued so far on the two background streams. */
 OASIS_API oasis_status oasis_pipeline_join(oasis_pipeline* pipeline, void* stream);
 
-/* Profile the next max_steps steps: timing events are recorded around each
- * kernel on the stream it runs on (attention incl. its merge on the foreground;
+/* Profile the next max_steps steps: each kernel launch carries timing events
+ * that take the start and end timestamps of its own dispatch, on the stream it
+ * runs on (attention from its split kernel's start to its merge kernel's end on the foreground;
  * scoring and top-K on the prediction stream; staging on the transfer stream).
  * The events are created here, not in the steps. */
 OASIS_API oasis_status oasis_pipeline_profile_begin(oasis_pipeline* pipeline, int32_t max_steps);

@@ -415,24 +415,28 @@ __global__ __launch_bounds__(kHeadDim) void attn_merge_kernel(AttnArgs a) {
 }
 
 template <int NT, int BS>
-hipError_t launch_t(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_t(const AttnArgs& a, hipStream_t s, const LaunchTiming& t) {
   const int nrh = a.R * a.Hkv;
   const int nrh8 = (nrh + 7) / 8 * 8;
-  hipLaunchKernelGGL((attn_split_kernel<NT, BS>), dim3((unsigned)(nrh8 * a.nsplit)), dim3(kW * 64), 0, s, a);
+  const bool merge = a.nsplit > 1;
+  // timed as one span: from the split kernel's start to the merge kernel's end
+  launch_kernel(attn_split_kernel<NT, BS>, dim3((unsigned)(nrh8 * a.nsplit)), dim3(kW * 64), s,
+                LaunchTiming{t.start, merge ? nullptr : t.stop}, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.nsplit == 1) return e;
-  hipLaunchKernelGGL(attn_merge_kernel, dim3((unsigned)a.rows, (unsigned)nrh), dim3(kHeadDim), 0, s, a);
+  if (e != hipSuccess || !merge) return e;
+  launch_kernel(attn_merge_kernel, dim3((unsigned)a.rows, (unsigned)nrh), dim3(kHeadDim), s,
+                LaunchTiming{nullptr, t.stop}, a);
   return hipGetLastError();
 }
 
 template <int BS>
-hipError_t launch_bs(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_bs(const AttnArgs& a, hipStream_t s, const LaunchTiming& t) {
   switch ((a.rows + 15) / 16) {
-    case 1: return launch_t<1, BS>(a, s);
-    case 2: return launch_t<2, BS>(a, s);
-    case 3: return launch_t<3, BS>(a, s);
-    case 4: return launch_t<4, BS>(a, s);
-    case 5: return launch_t<5, BS>(a, s);
+    case 1: return launch_t<1, BS>(a, s, t);
+    case 2: return launch_t<2, BS>(a, s, t);
+    case 3: return launch_t<3, BS>(a, s, t);
+    case 4: return launch_t<4, BS>(a, s, t);
+    case 5: return launch_t<5, BS>(a, s, t);
     default: return hipErrorInvalidValue;
   }
 }
@@ -459,8 +463,8 @@ AttnPlan attn_plan(int R, int Hq, int Hkv, int T, int B, int k_slots) {
   return p;
 }
 
-hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
-  return a.B == 16 ? launch_bs<16>(a, s) : launch_bs<32>(a, s);
+hipError_t launch_attn(const AttnArgs& a, hipStream_t s, const LaunchTiming& t) {
+  return a.B == 16 ? launch_bs<16>(a, s, t) : launch_bs<32>(a, s, t);
 }
 
 }  // namespace oasis

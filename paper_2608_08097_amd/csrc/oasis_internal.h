@@ -1,6 +1,7 @@
 // Internal declarations of the OasisKV HIP library (gfx950 / MI355X).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -46,6 +47,21 @@ __device__ __forceinline__ Ctx ctx_blocks(int L, int B, int max_blocks) {
 
 // --- host-side launchers (one per .hip translation unit) ---------------------
 
+// Optional timing of one launch: when set, the events take the start / end
+// timestamps of the kernel dispatch itself (not of a marker next to it).
+struct LaunchTiming {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
+template <typename F, typename... Args>
+inline void launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t s, const LaunchTiming& t, Args... args) {
+  if (t.start || t.stop)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, t.start, t.stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+}
+
 struct SummaryArgs {
   const uint16_t* k_pages;
   int64_t num_pages;
@@ -65,7 +81,7 @@ struct ScoreArgs {
   float* scores;
   int R, Hq, Hkv, G, T, first_draft, num_draft, B, NBmax;
 };
-hipError_t launch_score(const ScoreArgs& a, hipStream_t s);
+hipError_t launch_score(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t = {});
 
 struct TopkArgs {
   const float* scores;
@@ -74,7 +90,7 @@ struct TopkArgs {
   int32_t* sel_count;
   int R, Hkv, B, NBmax, k;
 };
-hipError_t launch_topk(const TopkArgs& a, hipStream_t s);
+hipError_t launch_topk(const TopkArgs& a, hipStream_t s, const LaunchTiming& t = {});
 
 struct StageArgs {
   const uint16_t* host_k;   // device-visible addresses
@@ -94,7 +110,7 @@ struct StageArgs {
   int fetch_cap;            // admitted misses per (request, KV head), >= k: all
   int local_only;           // no selection: refresh the local block only
 };
-hipError_t launch_stage(const StageArgs& a, hipStream_t s);
+hipError_t launch_stage(const StageArgs& a, hipStream_t s, const LaunchTiming& t = {});
 
 struct AttnArgs {
   const uint16_t* q;
@@ -115,7 +131,7 @@ struct AttnPlan {
   size_t part_o_floats, part_ml_floats, bytes;
 };
 AttnPlan attn_plan(int R, int Hq, int Hkv, int T, int B, int k_slots);
-hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn(const AttnArgs& a, hipStream_t s, const LaunchTiming& t = {});
 
 // --- argument checks shared by the entry points (api.hip) ---------------------
 // Each builder validates like the entry point of the same operation (fn names

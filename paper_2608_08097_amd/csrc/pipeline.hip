@@ -91,10 +91,11 @@ void drop_profile(oasis_pipeline* p) {
   p->prof_cap = p->prof_n = 0;
 }
 
-// Timing event `end` (0 = before, 1 = after) of kernel kind `kind` in the current profiled step.
-hipError_t prof_mark(oasis_pipeline* p, int kind, int end, hipStream_t s) {
-  if (!p->prof_ev || p->prof_n >= p->prof_cap) return hipSuccess;
-  return hipEventRecord(p->prof_ev[(p->prof_n * kProfKinds + kind) * 2 + end], s);
+// Dispatch timing of kernel kind `kind` in the current profiled step (none when not profiling).
+oasis::LaunchTiming prof_timing(oasis_pipeline* p, int kind) {
+  if (!p->prof_ev || p->prof_n >= p->prof_cap) return {};
+  hipEvent_t* e = p->prof_ev + (p->prof_n * kProfKinds + kind) * 2;
+  return oasis::LaunchTiming{e[0], e[1]};
 }
 
 void release(oasis_pipeline* p) {
@@ -259,22 +260,14 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   HIP_TRY(signal(p, fg, kQ, ++cnt[kQ]), fn);
   HIP_TRY(wait_for(p, p->pred, kQ, cnt[kQ]), fn);
   if (growing) HIP_TRY(oasis::launch_stage(la, fg), fn);
-  HIP_TRY(prof_mark(p, 0, 0, fg), fn);
-  HIP_TRY(oasis::launch_attn(aa, fg), fn);
-  HIP_TRY(prof_mark(p, 0, 1, fg), fn);
+  HIP_TRY(oasis::launch_attn(aa, fg, prof_timing(p, 0)), fn);
   HIP_TRY(signal(p, fg, kAttn, ++cnt[kAttn]), fn);
-  HIP_TRY(prof_mark(p, 1, 0, p->pred), fn);
-  HIP_TRY(oasis::launch_score(sa, p->pred), fn);
-  HIP_TRY(prof_mark(p, 1, 1, p->pred), fn);
-  HIP_TRY(prof_mark(p, 2, 0, p->pred), fn);
-  HIP_TRY(oasis::launch_topk(ta, p->pred), fn);
-  HIP_TRY(prof_mark(p, 2, 1, p->pred), fn);
+  HIP_TRY(oasis::launch_score(sa, p->pred, prof_timing(p, 1)), fn);
+  HIP_TRY(oasis::launch_topk(ta, p->pred, prof_timing(p, 2)), fn);
   HIP_TRY(signal(p, p->pred, kPred, ++cnt[kPred]), fn);
   HIP_TRY(wait_for(p, p->xfer, kPred, cnt[kPred]), fn);
   HIP_TRY(wait_for(p, p->xfer, kAttn, cnt[kAttn]), fn);  // the gather overwrites slots the attention reads
-  HIP_TRY(prof_mark(p, 3, 0, p->xfer), fn);
-  HIP_TRY(oasis::launch_stage(ga, p->xfer), fn);
-  HIP_TRY(prof_mark(p, 3, 1, p->xfer), fn);
+  HIP_TRY(oasis::launch_stage(ga, p->xfer, prof_timing(p, 3)), fn);
   HIP_TRY(signal(p, p->xfer, sl, ++p->staged[layer]), fn);
   if (p->prof_ev && p->prof_n < p->prof_cap) ++p->prof_n;
   return ok();

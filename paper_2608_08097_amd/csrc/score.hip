@@ -112,22 +112,22 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
 }
 
 template <int NRT, int TPW>
-hipError_t launch_t(const ScoreArgs& a, hipStream_t s) {
+hipError_t launch_t(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t) {
   const int ntiles = (a.NBmax + 15) / 16;
   const dim3 grid((unsigned)((ntiles + 4 * TPW - 1) / (4 * TPW)), (unsigned)(a.R * a.Hkv));
-  hipLaunchKernelGGL((score_kernel<NRT, TPW>), grid, dim3(256), 0, s, a);
+  launch_kernel(score_kernel<NRT, TPW>, grid, dim3(256), s, t, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
+hipError_t launch_score(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t) {
   const int rows = a.num_draft * a.G;
   switch ((rows + 15) / 16) {
-    case 1: return launch_t<1, 4>(a, s);
-    case 2: return launch_t<2, 4>(a, s);
-    case 3: return launch_t<3, 2>(a, s);
-    case 4: return launch_t<4, 2>(a, s);
+    case 1: return launch_t<1, 4>(a, s, t);
+    case 2: return launch_t<2, 4>(a, s, t);
+    case 3: return launch_t<3, 2>(a, s, t);
+    case 4: return launch_t<4, 2>(a, s, t);
     default: return hipErrorInvalidValue;
   }
 }

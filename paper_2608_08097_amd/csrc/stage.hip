@@ -336,23 +336,23 @@ __global__ __launch_bounds__(kPlanThreads) void stage_kernel(StageArgs a) {
 }  // namespace
 
 template <int BS>
-hipError_t launch_bs(const StageArgs& a, hipStream_t s) {
+hipError_t launch_bs(const StageArgs& a, hipStream_t s, const LaunchTiming& t) {
   const int nrh = a.R * a.Hkv;
   const int grid = nrh < kCopyWorkgroups ? nrh : kCopyWorkgroups;
   const int pf = kCopyInflight / grid;  // entries per workgroup batch
   if (pf >= 8)
-    hipLaunchKernelGGL((stage_kernel<BS, 8>), dim3(grid), dim3(kPlanThreads), 0, s, a);
+    launch_kernel(stage_kernel<BS, 8>, dim3(grid), dim3(kPlanThreads), s, t, a);
   else if (pf >= 4)
-    hipLaunchKernelGGL((stage_kernel<BS, 4>), dim3(grid), dim3(kPlanThreads), 0, s, a);
+    launch_kernel(stage_kernel<BS, 4>, dim3(grid), dim3(kPlanThreads), s, t, a);
   else if (pf >= 2)
-    hipLaunchKernelGGL((stage_kernel<BS, 2>), dim3(grid), dim3(kPlanThreads), 0, s, a);
+    launch_kernel(stage_kernel<BS, 2>, dim3(grid), dim3(kPlanThreads), s, t, a);
   else
-    hipLaunchKernelGGL((stage_kernel<BS, 1>), dim3(grid), dim3(kPlanThreads), 0, s, a);
+    launch_kernel(stage_kernel<BS, 1>, dim3(grid), dim3(kPlanThreads), s, t, a);
   return hipGetLastError();
 }
 
-hipError_t launch_stage(const StageArgs& a, hipStream_t s) {
-  return a.B == 16 ? launch_bs<16>(a, s) : launch_bs<32>(a, s);
+hipError_t launch_stage(const StageArgs& a, hipStream_t s, const LaunchTiming& t) {
+  return a.B == 16 ? launch_bs<16>(a, s, t) : launch_bs<32>(a, s, t);
 }
 
 }  // namespace oasis

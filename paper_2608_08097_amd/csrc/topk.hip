@@ -183,18 +183,18 @@ __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
 
 }  // namespace
 
-hipError_t launch_topk(const TopkArgs& a, hipStream_t s) {
+hipError_t launch_topk(const TopkArgs& a, hipStream_t s, const LaunchTiming& t) {
   // the candidate count of every request is at most NBmax - 1
   const int per = (a.NBmax + kThreads - 1) / kThreads;
   const dim3 grid((unsigned)(a.R * a.Hkv));
   if (per <= 8)
-    hipLaunchKernelGGL(topk_kernel<8>, grid, dim3(kThreads), 0, s, a);
+    launch_kernel(topk_kernel<8>, grid, dim3(kThreads), s, t, a);
   else if (per <= 16)
-    hipLaunchKernelGGL(topk_kernel<16>, grid, dim3(kThreads), 0, s, a);
+    launch_kernel(topk_kernel<16>, grid, dim3(kThreads), s, t, a);
   else if (per <= 32)
-    hipLaunchKernelGGL(topk_kernel<32>, grid, dim3(kThreads), 0, s, a);
+    launch_kernel(topk_kernel<32>, grid, dim3(kThreads), s, t, a);
   else
-    hipLaunchKernelGGL(topk_kernel<0>, grid, dim3(kThreads), 0, s, a);
+    launch_kernel(topk_kernel<0>, grid, dim3(kThreads), s, t, a);
   return hipGetLastError();
 }
 

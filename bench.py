@@ -80,6 +80,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention comparison")
+    ap.add_argument("--fetch-sweep", action="store_true",
+                    help="step rate and bytes per step for fetch ratios 0.01 .. 0.2 and uncapped (Tab. eviction)")
     ap.add_argument("--kernels-only", action="store_true",
                     help="only time the kernels alone on one stream (for hardware-counter passes)")
     ap.add_argument("--copy-calib", action="store_true",
@@ -202,6 +204,11 @@ def main():
         st.kmin.copy_(layers[0].kmin)
     qs = [[torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16) for x in w.layer_queries(l, per_layer_steps)]
           for l in range(NL)]
+    if args.fetch_sweep:
+        path.close()
+        print(json.dumps({"fetch_sweep": fetch_sweep(P, torch, DecodePath, d, c, K, hk_t, hv_t, bt, layers, qs,
+                                                     ctx_d, args)}), flush=True)
+        return
     # The working set a layer holds when decoding starts: one uncapped fill from
     # its first prediction (untimed; decode steps are then capped).
     for l, st in enumerate(layers):
@@ -312,6 +319,51 @@ def main():
         log("timing the oracle sample")
         result["cpu_baseline"] = cpu_baseline(w, hk, hv, w.layer_queries(0, 64), K, fetch_cap, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def fetch_sweep(P, torch, DecodePath, d, c, K, hk_t, hv_t, bt, layers, qs, ctx_d, args):
+    """The fetch-cap ablation of §5.5.1 on this workload: for each ratio, the same
+    steps from the same initial fill; entries and bytes moved per step, the step
+    rate, and the host-to-device rate the staging sustains at that step rate."""
+    NL = len(layers)
+    entry_bytes = 2 * c.block_size * c.head_dim * 2
+    out = []
+    for ratio in (0.01, 0.02, 0.05, 0.10, 0.20, 1.0):
+        cap = K if ratio >= 1.0 else max(1, int(math.floor(ratio * K)))
+        path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=cap)
+        for l, st in enumerate(layers):
+            st.reset()
+            path.predict(st, qs[l][0], ctx_d)
+            path.stage(st, ctx_d, 0, fetch_cap=K)
+        moved = torch.zeros((args.steps, c.num_reqs, c.num_kv_heads), dtype=torch.int32, device="cuda")
+        torch.cuda.synchronize()
+        for i in range(args.warmup):
+            path.step_pipelined(layers[i % NL], qs[i % NL][i // NL], ctx_d, i)
+        path.join()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.warmup, args.warmup + args.steps):
+            path.step_pipelined(layers[i % NL], qs[i % NL][i // NL], ctx_d, i, moved=moved[i - args.warmup])
+        path.join()
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        n_prof = min(64, args.steps)
+        path.profile_begin(n_prof)
+        for i in range(args.warmup + args.steps, args.warmup + args.steps + n_prof):
+            path.step_pipelined(layers[i % NL], qs[i % NL][i // NL], ctx_d, i)
+        path.join()
+        torch.cuda.synchronize()
+        prof, _ = path.profile_end()
+        path.close()
+        entries = float(moved.sum().item()) / args.steps
+        rate = args.steps / el
+        row = {"fetch_ratio": ratio if cap < K else "all", "fetch_cap": cap, "entries_per_step": round(entries, 1),
+               "MB_per_step": round(entries * entry_bytes / 1e6, 3), "steps_per_s": round(rate, 1),
+               "h2d_GBs_at_step_rate": round(entries * entry_bytes * rate / 1e9, 2),
+               "pipeline_kernel_us": {k_: round(v, 1) for k_, v in prof.items()}}
+        log(f"fetch sweep {row}")
+        out.append(row)
+    return out
 
 
 def isolated(P, torch, path, layers, qs, ctx_d, iters=64):

@@ -96,6 +96,65 @@ def block_summaries(host_k, block_table, ctx_len, block_size: int, nb_max: int):
     return kmax, kmin
 
 
+def update_summaries(host_k, block_table, prev_ctx_len, ctx_len, block_size: int, kmax, kmin,
+                     max_new_blocks: int | None = None):
+    """Compressed keys of the blocks completed since ``prev_ctx_len``; in place.
+
+    Paper §5.1 lists compressed-key updates among the native operations: as the
+    context grows, each logical block that fills up gets its min/max rows
+    (§4.2.1), and earlier rows stay as they are. Here, per request, the rows of
+    candidate blocks [n_cand(prev), n_cand(cur)) are written, at most
+    ``max_new_blocks`` of them from the first; every other row is untouched.
+    Returns the number of rows written per request.
+    """
+    host_k = np.asarray(host_k)
+    _, Hkv, B, d = host_k.shape
+    assert B == block_size
+    written = np.zeros(len(ctx_len), np.int32)
+    for r in range(len(ctx_len)):
+        _, lo, _ = block_counts(prev_ctx_len[r], B)
+        _, hi, _ = block_counts(ctx_len[r], B)
+        if max_new_blocks is not None:
+            hi = min(hi, lo + max_new_blocks)
+        for b in range(lo, hi):
+            keys = bf16_to_f64(host_k[int(block_table[r][b])])   # [Hkv][B][d]
+            kmax[r, :, b, :] = keys.max(axis=1)
+            kmin[r, :, b, :] = keys.min(axis=1)
+            written[r] += 1
+    return written
+
+
+def copy_blocks(src_k, src_v, src_table, dst_k, dst_v, dst_table, prev_ctx_len, ctx_len, block_size: int,
+                max_blocks: int | None = None):
+    """Copy the logical blocks touched by tokens [prev, cur) between two paged tiers; in place.
+
+    Paper §4.3: once a request's context passes the sparsification threshold,
+    its whole KV cache is copied to CPU memory (the full tier) and only the
+    selected blocks and the local window stay on the GPU; after that, newly
+    written tokens must reach the full tier as well. Both are this copy: with
+    prev = 0 every block of the context (the partial local block included); with
+    the previous length, the blocks that received new tokens. Pages hold every
+    KV head of a block ([Hkv][B][d], §4.3 Head-Token-Dimension order); at most
+    ``max_blocks`` blocks are copied per request, from the first.
+    Returns the number of blocks copied per request.
+    """
+    B = block_size
+    copied = np.zeros(len(ctx_len), np.int32)
+    for r in range(len(ctx_len)):
+        prev, cur = int(prev_ctx_len[r]), int(ctx_len[r])
+        if cur <= prev:
+            continue
+        lo, hi = prev // B, (cur + B - 1) // B
+        if max_blocks is not None:
+            hi = min(hi, lo + max_blocks)
+        for b in range(lo, hi):
+            s, t = int(src_table[r][b]), int(dst_table[r][b])
+            dst_k[t] = src_k[s]
+            dst_v[t] = src_v[s]
+            copied[r] += 1
+    return copied
+
+
 # ---------------------------------------------------------------------------
 # O1: block importance from the draft queries
 # ---------------------------------------------------------------------------

@@ -397,6 +397,84 @@ def test_stage_capped_converges():
 
 
 # ---------------------------------------------------------------------------
+# Growth of the context: summary updates and block copies between tiers
+# ---------------------------------------------------------------------------
+
+def test_update_summaries_matches_full_build_along_growth():
+    """Updating on every append reproduces the full build (§4.2.1 summaries, §5.1 updates)."""
+    rng = np.random.default_rng(21)
+    R, H, B, d, NB = 3, 2, 4, 8, 40
+    keys = rng.integers(0, 2 ** 16, size=(R * NB, H, B, d), dtype=np.uint16) & np.uint16(0x7F7F)  # finite bf16
+    bt = rng.permutation(R * NB).reshape(R, NB).astype(np.int32)
+    kmax = np.full((R, H, NB, d), np.nan)
+    kmin = np.full((R, H, NB, d), np.nan)
+    ctx = np.zeros(R, np.int32)
+    for step in range(25):
+        prev = ctx.copy()
+        ctx = np.minimum(ctx + rng.integers(0, 3 * B, size=R), NB * B).astype(np.int32)
+        n = O.update_summaries(keys, bt, prev, ctx, B, kmax, kmin)
+        ref_max, ref_min = O.block_summaries(keys, bt, ctx, B, NB)
+        for r in range(R):
+            nc = O.block_counts(ctx[r], B)[1]
+            assert n[r] == nc - O.block_counts(prev[r], B)[1]
+            assert np.array_equal(kmax[r, :, :nc], ref_max[r, :, :nc])
+            assert np.array_equal(kmin[r, :, :nc], ref_min[r, :, :nc])
+            assert np.isnan(kmax[r, :, nc:]).all()        # the local block and beyond: not yet summarised
+    # a bound below the growth writes only the first rows
+    kmax2 = np.full_like(kmax, np.nan)
+    kmin2 = np.full_like(kmin, np.nan)
+    n = O.update_summaries(keys, bt, np.zeros(R, np.int32), np.full(R, 10 * B + 1, np.int32), B, kmax2, kmin2,
+                           max_new_blocks=3)
+    assert list(n) == [3] * R
+    assert not np.isnan(kmax2[:, :, :3]).any() and np.isnan(kmax2[:, :, 3:]).all()
+
+
+@pytest.mark.parametrize("prev,cur,expect", [(0, 1, [0]), (0, 33, [0, 1, 2]), (32, 33, [2]), (31, 33, [1, 2]),
+                                             (16, 16, []), (20, 19, []), (5, 48, [0, 1, 2])])
+def test_copy_blocks_touched_range(prev, cur, expect):
+    """Blocks copied = those holding tokens [prev, cur): ceil(cur/B) - floor(prev/B) of them (§4.3)."""
+    B, H, d, NB = 16, 2, 4, 8
+    rng = np.random.default_rng(prev * 100 + cur)
+    src_k = rng.integers(0, 2 ** 16, size=(NB, H, B, d), dtype=np.uint16)
+    src_v = rng.integers(0, 2 ** 16, size=(NB, H, B, d), dtype=np.uint16)
+    st = rng.permutation(NB).astype(np.int32)[None]
+    dt = rng.permutation(NB).astype(np.int32)[None]
+    dst_k = np.zeros_like(src_k)
+    dst_v = np.zeros_like(src_v)
+    n = O.copy_blocks(src_k, src_v, st, dst_k, dst_v, dt, np.array([prev]), np.array([cur]), B)
+    assert n[0] == len(expect)
+    for b in range(NB):
+        if b in expect:
+            assert np.array_equal(dst_k[dt[0, b]], src_k[st[0, b]]) and np.array_equal(dst_v[dt[0, b]], src_v[st[0, b]])
+        else:
+            assert not dst_k[dt[0, b]].any() and not dst_v[dt[0, b]].any()
+
+
+def test_transition_then_staging_equals_staging_from_the_device_tier():
+    """Dense -> sparse (§4.3): after copying the whole context to the host tier, staging the
+    selection from it gives the same working set as staging from the device pages."""
+    w = Workload(tiny_cfg(num_reqs=2, ctx_args=(40, 90)))
+    c = w.cfg
+    hk, hv, ctx, kmax, kmin = _summaries(w)
+    K = c.K
+    dev_bt = w.block_table
+    n_host = c.num_reqs * w.NBmax                     # a host tier of its own, pages in another order
+    host_bt = np.random.default_rng(3).permutation(n_host).reshape(c.num_reqs, w.NBmax).astype(np.int32)
+    host_k = np.zeros((n_host,) + hk.shape[1:], hk.dtype)
+    host_v = np.zeros_like(host_k)
+    n = O.copy_blocks(hk, hv, dev_bt, host_k, host_v, host_bt, np.zeros(c.num_reqs, np.int32), ctx, c.block_size)
+    assert list(n) == [O.block_counts(L, c.block_size)[0] for L in ctx]
+    s = O.block_scores(w.queries(0), kmax, kmin, ctx, c.num_kv_heads, c.block_size)
+    sel, cnt = O.select_topk(s, ctx, K, c.block_size)
+    pools = []
+    for src_k, src_v, bt in ((hk, hv, dev_bt), (host_k, host_v, host_bt)):
+        smap, stamp, pk, pv = _empty_state(c.num_reqs, c.num_kv_heads, K, c.block_size, c.head_dim)
+        O.stage_blocks(src_k, src_v, bt, sel, cnt, smap, stamp, 0, pk, pv, ctx, c.block_size)
+        pools.append((smap, pk, pv))
+    assert all(np.array_equal(a, b) for a, b in zip(pools[0], pools[1]))
+
+
+# ---------------------------------------------------------------------------
 # O4 attention
 # ---------------------------------------------------------------------------
 

@@ -135,7 +135,8 @@ def copy_blocks(src_k, src_v, src_table, dst_k, dst_v, dst_table, prev_ctx_len, 
     prev = 0 every block of the context (the partial local block included); with
     the previous length, the blocks that received new tokens. Pages hold every
     KV head of a block ([Hkv][B][d], §4.3 Head-Token-Dimension order); at most
-    ``max_blocks`` blocks are copied per request, from the first.
+    ``max_blocks`` blocks are copied per request, from the first. A block whose
+    page id in either table is negative (no page) is skipped (reading R24).
     Returns the number of blocks copied per request.
     """
     B = block_size
@@ -147,8 +148,10 @@ def copy_blocks(src_k, src_v, src_table, dst_k, dst_v, dst_table, prev_ctx_len, 
         lo, hi = prev // B, (cur + B - 1) // B
         if max_blocks is not None:
             hi = min(hi, lo + max_blocks)
-        for b in range(lo, hi):
+        for b in range(lo, min(hi, len(src_table[r]))):
             s, t = int(src_table[r][b]), int(dst_table[r][b])
+            if s < 0 or t < 0:
+                continue
             dst_k[t] = src_k[s]
             dst_v[t] = src_v[s]
             copied[r] += 1

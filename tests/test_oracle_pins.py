@@ -450,6 +450,23 @@ def test_copy_blocks_touched_range(prev, cur, expect):
             assert not dst_k[dt[0, b]].any() and not dst_v[dt[0, b]].any()
 
 
+def test_copy_blocks_skips_blocks_without_pages():
+    """A block with no page (-1) in either table is not copied, and nothing else is touched."""
+    B, H, d = 4, 1, 2
+    src_k = np.arange(6 * H * B * d, dtype=np.uint16).reshape(6, H, B, d)
+    src_v = src_k + np.uint16(1000)
+    st = np.array([[0, 1, -1, 3, 4, 5]], np.int32)
+    dt = np.array([[5, -1, 3, 2, 1, 0]], np.int32)
+    dst_k = np.zeros_like(src_k)
+    dst_v = np.zeros_like(src_v)
+    n = O.copy_blocks(src_k, src_v, st, dst_k, dst_v, dt, np.array([0]), np.array([6 * B]), B)
+    assert n[0] == 4                                   # blocks 1 (no destination) and 2 (no source) skipped
+    for b, (s_, t_) in enumerate(zip(st[0], dt[0])):
+        if s_ >= 0 and t_ >= 0:
+            assert np.array_equal(dst_k[t_], src_k[s_]) and np.array_equal(dst_v[t_], src_v[s_])
+    assert not dst_k[3].any()                          # block 2's destination page stays untouched
+
+
 def test_transition_then_staging_equals_staging_from_the_device_tier():
     """Dense -> sparse (§4.3): after copying the whole context to the host tier, staging the
     selection from it gives the same working set as staging from the device pages."""

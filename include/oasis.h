@@ -9,8 +9,12 @@
  *   oasis_stage_blocks       delta-select and gather them from pinned host   (§4.2.3, §4.3, §5.1)
  *   oasis_sparse_decode_attn attention of the stacked queries over them      (§4.2.1, §4.3, §5.2)
  *
- * plus oasis_build_summaries, which makes the compressed keys the scorer reads
- * (§4.2.1, "Look-ahead attention" figure) once per completed block.
+ * plus oasis_build_summaries / oasis_update_summaries, which make the
+ * compressed keys the scorer reads (§4.2.1, "Look-ahead attention" figure; §5.1)
+ * for the whole context or for the blocks completed since the last call;
+ * oasis_copy_blocks, which moves blocks between the GPU pages and the full host
+ * tier (§4.3, dense-to-sparse transition and appends); and oasis_pipeline_*,
+ * the native issuer of the layer-pipelined step (§4.2.2).
  *
  * General conventions
  * -------------------
@@ -112,6 +116,45 @@ OASIS_API int32_t oasis_abi_version(void);
 OASIS_API oasis_status oasis_build_summaries(const oasis_dims* dims, const uint16_t* k_pages, int64_t num_pages,
                                    const int32_t* block_table, const int32_t* ctx_len,
                                    uint16_t* kmax, uint16_t* kmin, void* stream);
+
+/*
+ * Compressed-key update on append (paper §5.1 lists compressed-key updates
+ * among the native operations; §4.2.1 defines the rows). For every request r:
+ * the rows of the candidate blocks completed since prev_ctx_len[r], i.e.
+ * b in [n_cand(prev_ctx_len[r]), n_cand(ctx_len[r])), at most max_new_blocks
+ * of them from the first, are written as oasis_build_summaries writes them;
+ * every other row is untouched. ctx_len[r] <= prev_ctx_len[r] writes nothing.
+ * A caller appending one token per step passes max_new_blocks = 1; a bound
+ * below a request's growth leaves its later rows unwritten.
+ * k_pages: device memory or pinned host memory; everything else: device.
+ */
+OASIS_API oasis_status oasis_update_summaries(const oasis_dims* dims, const uint16_t* k_pages, int64_t num_pages,
+                                    const int32_t* block_table, const int32_t* prev_ctx_len,
+                                    const int32_t* ctx_len, int32_t max_new_blocks,
+                                    uint16_t* kmax, uint16_t* kmin, void* stream);
+
+/*
+ * Block copy between two paged KV tiers (paper §4.3: once a request's context
+ * passes the sparsification threshold, its whole KV cache is copied to CPU
+ * memory while the GPU keeps only the selected blocks and the local window;
+ * blocks that receive new tokens afterwards must reach the full tier as well).
+ * For every request r, the logical blocks holding tokens
+ * [prev_ctx_len[r], ctx_len[r]) (prev_ctx_len NULL: from 0) are copied, at most
+ * max_blocks of them from the first: page src_block_table[r][b] of src_k/src_v
+ * to page dst_block_table[r][b] of dst_k/dst_v, all KV heads of the page
+ * ([Hkv][B][d] each). Blocks past max_blocks of the table, or pages outside
+ * [0, num_*_pages), are skipped. The dense-to-sparse transition is one call
+ * with prev_ctx_len = NULL from the device pages to the pinned host tier,
+ * followed by oasis_stage_blocks from the device pages (still resident) into
+ * empty slots. src/dst: device memory or pinned host memory (device-visible;
+ * the library resolves the address); block tables and lengths: device.
+ * 1 <= max_blocks <= 65535.
+ */
+OASIS_API oasis_status oasis_copy_blocks(const oasis_dims* dims, const uint16_t* src_k, const uint16_t* src_v,
+                               int64_t num_src_pages, const int32_t* src_block_table,
+                               uint16_t* dst_k, uint16_t* dst_v, int64_t num_dst_pages,
+                               const int32_t* dst_block_table, const int32_t* prev_ctx_len,
+                               const int32_t* ctx_len, int32_t max_blocks, void* stream);
 
 /*
  * Block importance from the lookahead (draft) queries (paper §4.2.1: each

@@ -21,7 +21,8 @@ STATUS = {0: "OASIS_OK", 1: "OASIS_ERR_INVALID_ARG", 2: "OASIS_ERR_UNSUPPORTED",
           3: "OASIS_ERR_HIP", 4: "OASIS_ERR_WORKSPACE"}
 
 EXPORTS = (
-    "oasis_last_error", "oasis_abi_version", "oasis_build_summaries", "oasis_score_blocks",
+    "oasis_last_error", "oasis_abi_version", "oasis_build_summaries", "oasis_update_summaries",
+    "oasis_copy_blocks", "oasis_score_blocks",
     "oasis_select_topk", "oasis_stage_blocks",
     "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn",
     "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_step", "oasis_pipeline_join",
@@ -78,6 +79,10 @@ def lib() -> ctypes.CDLL:
         L.oasis_abi_version.argtypes = []
         L.oasis_build_summaries.restype = _I32
         L.oasis_build_summaries.argtypes = [_DIMS, _P, _I64, _P, _P, _P, _P, _P]
+        L.oasis_update_summaries.restype = _I32
+        L.oasis_update_summaries.argtypes = [_DIMS, _P, _I64, _P, _P, _P, _I32, _P, _P, _P]
+        L.oasis_copy_blocks.restype = _I32
+        L.oasis_copy_blocks.argtypes = [_DIMS, _P, _P, _I64, _P, _P, _P, _I64, _P, _P, _P, _I32, _P]
         L.oasis_score_blocks.restype = _I32
         L.oasis_score_blocks.argtypes = [_DIMS, _P, _I32, _I32, _I32, _P, _P, _P, _P, _P]
         L.oasis_select_topk.restype = _I32
@@ -176,6 +181,42 @@ def oasis_build_summaries(d: OasisDims, k_pages, block_table, ctx_len, kmax, kmi
         ctypes.byref(d), _host_or_dev(k_pages, "k_pages", _BF16), int(k_pages.shape[0]),
         _dev(block_table, "block_table", _I32T), _dev(ctx_len, "ctx_len", _I32T),
         _dev(kmax, "kmax", _BF16), _dev(kmin, "kmin", _BF16), _stream(stream)))
+
+
+def oasis_update_summaries(d: OasisDims, k_pages, block_table, prev_ctx_len, ctx_len, max_new_blocks: int,
+                           kmax, kmin, stream=None) -> None:
+    R, H, NB, D = d.num_reqs, d.num_kv_heads, d.max_blocks, d.head_dim
+    _need(k_pages, k_pages.shape[0] * H * d.block_size * D, "k_pages")
+    _need(block_table, R * NB, "block_table")
+    _need(prev_ctx_len, R, "prev_ctx_len")
+    _need(ctx_len, R, "ctx_len")
+    _need(kmax, R * H * NB * D, "kmax")
+    _need(kmin, R * H * NB * D, "kmin")
+    _check("oasis_update_summaries", lib().oasis_update_summaries(
+        ctypes.byref(d), _host_or_dev(k_pages, "k_pages", _BF16), int(k_pages.shape[0]),
+        _dev(block_table, "block_table", _I32T), _dev(prev_ctx_len, "prev_ctx_len", _I32T),
+        _dev(ctx_len, "ctx_len", _I32T), int(max_new_blocks), _dev(kmax, "kmax", _BF16), _dev(kmin, "kmin", _BF16),
+        _stream(stream)))
+
+
+def oasis_copy_blocks(d: OasisDims, src_k, src_v, src_block_table, dst_k, dst_v, dst_block_table, prev_ctx_len,
+                      ctx_len, max_blocks: int, stream=None) -> None:
+    R, H, NB, D, B = d.num_reqs, d.num_kv_heads, d.max_blocks, d.head_dim, d.block_size
+    for t, name in ((src_k, "src_k"), (src_v, "src_v"), (dst_k, "dst_k"), (dst_v, "dst_v")):
+        if t.dim() < 1 or t.numel() % (H * B * D):
+            raise ValueError(f"{name}: not whole pages of [Hkv][B][d]")
+    if src_k.shape != src_v.shape or dst_k.shape != dst_v.shape:
+        raise ValueError("K and V tiers differ in shape")
+    _need(src_block_table, R * NB, "src_block_table")
+    _need(dst_block_table, R * NB, "dst_block_table")
+    _need(prev_ctx_len, R, "prev_ctx_len")
+    _need(ctx_len, R, "ctx_len")
+    _check("oasis_copy_blocks", lib().oasis_copy_blocks(
+        ctypes.byref(d), _host_or_dev(src_k, "src_k", _BF16), _host_or_dev(src_v, "src_v", _BF16),
+        src_k.numel() // (H * B * D), _dev(src_block_table, "src_block_table", _I32T),
+        _host_or_dev(dst_k, "dst_k", _BF16), _host_or_dev(dst_v, "dst_v", _BF16), dst_k.numel() // (H * B * D),
+        _dev(dst_block_table, "dst_block_table", _I32T), _dev(prev_ctx_len, "prev_ctx_len", _I32T, nullable=True),
+        _dev(ctx_len, "ctx_len", _I32T), int(max_blocks), _stream(stream)))
 
 
 def oasis_score_blocks(d: OasisDims, q, num_q_tokens: int, first_draft: int, num_draft: int,

@@ -255,8 +255,74 @@ oasis_status oasis_build_summaries(const oasis_dims* dims, const uint16_t* k_pag
   st = oasis::device_view(k_pages, &kp, "k_pages", fn);
   if (st != OASIS_OK) return st;
   oasis::SummaryArgs a{static_cast<const uint16_t*>(kp), num_pages, block_table, ctx_len, kmax, kmin,
-                       dims->num_reqs, dims->num_kv_heads, dims->block_size, dims->max_blocks};
+                       dims->num_reqs, dims->num_kv_heads, dims->block_size, dims->max_blocks, nullptr, 0};
   return hip_status(oasis::launch_summaries(a, static_cast<hipStream_t>(stream)), fn);
+}
+
+oasis_status oasis_update_summaries(const oasis_dims* dims, const uint16_t* k_pages, int64_t num_pages,
+                                    const int32_t* block_table, const int32_t* prev_ctx_len, const int32_t* ctx_len,
+                                    int32_t max_new_blocks, uint16_t* kmax, uint16_t* kmin, void* stream) {
+  static const char* fn = "oasis_update_summaries";
+  oasis_status st = oasis::check_dims(dims, fn);
+  if (st != OASIS_OK) return st;
+  if (max_new_blocks < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: max_new_blocks = %d < 1", fn, max_new_blocks);
+  if (num_pages < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: num_pages < 1", fn);
+  if (dims->num_reqs == 0) return ok();
+  REQUIRE_PTR(k_pages, fn);
+  REQUIRE_PTR(block_table, fn);
+  REQUIRE_PTR(prev_ctx_len, fn);
+  REQUIRE_PTR(ctx_len, fn);
+  REQUIRE_PTR(kmax, fn);
+  REQUIRE_PTR(kmin, fn);
+  const void* kp = nullptr;
+  st = oasis::device_view(k_pages, &kp, "k_pages", fn);
+  if (st != OASIS_OK) return st;
+  oasis::SummaryArgs a{static_cast<const uint16_t*>(kp), num_pages, block_table, ctx_len, kmax, kmin,
+                       dims->num_reqs, dims->num_kv_heads, dims->block_size, dims->max_blocks, prev_ctx_len,
+                       max_new_blocks};
+  return hip_status(oasis::launch_summaries(a, static_cast<hipStream_t>(stream)), fn);
+}
+
+oasis_status oasis_copy_blocks(const oasis_dims* dims, const uint16_t* src_k, const uint16_t* src_v,
+                               int64_t num_src_pages, const int32_t* src_block_table, uint16_t* dst_k, uint16_t* dst_v,
+                               int64_t num_dst_pages, const int32_t* dst_block_table, const int32_t* prev_ctx_len,
+                               const int32_t* ctx_len, int32_t max_blocks, void* stream) {
+  static const char* fn = "oasis_copy_blocks";
+  oasis_status st = oasis::check_dims(dims, fn);
+  if (st != OASIS_OK) return st;
+  if (max_blocks < 1 || max_blocks > 65535)
+    return fail(OASIS_ERR_INVALID_ARG, "%s: max_blocks = %d outside [1, 65535]", fn, max_blocks);
+  if (num_src_pages < 1 || num_dst_pages < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: a tier has no pages", fn);
+  if (dims->num_reqs == 0) return ok();
+  REQUIRE_PTR(src_k, fn);
+  REQUIRE_PTR(src_v, fn);
+  REQUIRE_PTR(src_block_table, fn);
+  REQUIRE_PTR(dst_k, fn);
+  REQUIRE_PTR(dst_v, fn);
+  REQUIRE_PTR(dst_block_table, fn);
+  REQUIRE_PTR(ctx_len, fn);
+  const void *sk = nullptr, *sv = nullptr, *dk = nullptr, *dv = nullptr;
+  if ((st = oasis::device_view(src_k, &sk, "src_k", fn)) != OASIS_OK) return st;
+  if ((st = oasis::device_view(src_v, &sv, "src_v", fn)) != OASIS_OK) return st;
+  if ((st = oasis::device_view(dst_k, &dk, "dst_k", fn)) != OASIS_OK) return st;
+  if ((st = oasis::device_view(dst_v, &dv, "dst_v", fn)) != OASIS_OK) return st;
+  oasis::CopyArgs a{};
+  a.src_k = static_cast<const uint16_t*>(sk);
+  a.src_v = static_cast<const uint16_t*>(sv);
+  a.num_src_pages = num_src_pages;
+  a.src_table = src_block_table;
+  a.dst_k = static_cast<uint16_t*>(const_cast<void*>(dk));
+  a.dst_v = static_cast<uint16_t*>(const_cast<void*>(dv));
+  a.num_dst_pages = num_dst_pages;
+  a.dst_table = dst_block_table;
+  a.prev_ctx_len = prev_ctx_len;
+  a.ctx_len = ctx_len;
+  a.R = dims->num_reqs;
+  a.Hkv = dims->num_kv_heads;
+  a.B = dims->block_size;
+  a.NBmax = dims->max_blocks;
+  a.max_blocks = max_blocks;
+  return hip_status(oasis::launch_copy_blocks(a, static_cast<hipStream_t>(stream)), fn);
 }
 
 oasis_status oasis_score_blocks(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens,

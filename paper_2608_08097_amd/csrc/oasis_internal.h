@@ -70,8 +70,25 @@ struct SummaryArgs {
   uint16_t* kmax;
   uint16_t* kmin;
   int R, Hkv, B, NBmax;
+  const int32_t* prev_ctx_len;  // NULL: every candidate block; else blocks completed since this length
+  int max_new;                  // with prev_ctx_len: at most this many rows per request
 };
 hipError_t launch_summaries(const SummaryArgs& a, hipStream_t s);
+
+struct CopyArgs {
+  const uint16_t* src_k;  // device-visible addresses, pages [num_pages][Hkv][B][d]
+  const uint16_t* src_v;
+  int64_t num_src_pages;
+  const int32_t* src_table;
+  uint16_t* dst_k;
+  uint16_t* dst_v;
+  int64_t num_dst_pages;
+  const int32_t* dst_table;
+  const int32_t* prev_ctx_len;  // NULL: from token 0
+  const int32_t* ctx_len;
+  int R, Hkv, B, NBmax, max_blocks;
+};
+hipError_t launch_copy_blocks(const CopyArgs& a, hipStream_t s);
 
 struct ScoreArgs {
   const uint16_t* q;

@@ -1,5 +1,7 @@
 // Compressed keys: per-block coordinate-wise min/max of the keys (paper §4.2.1,
-// "Look-ahead attention" figure; Quest-style summaries, two rows per block).
+// "Look-ahead attention" figure; Quest-style summaries, two rows per block),
+// built for every candidate block, or updated for the blocks completed since a
+// previous context length (§5.1 compressed-key updates).
 //
 // One thread owns 8 consecutive dimensions of one (request, block, KV head) and
 // walks the B tokens of the page with 16-byte loads; neighbouring threads cover
@@ -15,12 +17,14 @@ __global__ __launch_bounds__(256) void summaries_kernel(SummaryArgs a) {
   const int r = blockIdx.y;
   const long long item = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const int per_block = a.Hkv * (kHeadDim / 8);
-  const int b = (int)(item / per_block);
   const int rem = (int)(item % per_block);
   const int h = rem / (kHeadDim / 8);
   const int d0 = (rem % (kHeadDim / 8)) * 8;
   const Ctx c = ctx_blocks(a.ctx_len[r], a.B, a.NBmax);
-  if (b >= c.n_cand) return;
+  // update form: the grid covers max_new blocks per request, from the first one completed since prev
+  const int lo = a.prev_ctx_len ? ctx_blocks(a.prev_ctx_len[r], a.B, a.NBmax).n_cand : 0;
+  const int b = lo + (int)(item / per_block);
+  if (b >= c.n_cand || (a.prev_ctx_len && b >= lo + a.max_new)) return;
   const int page = a.block_table[(long long)r * a.NBmax + b];
   if (page < 0 || page >= a.num_pages) return;
 
@@ -58,7 +62,8 @@ __global__ __launch_bounds__(256) void summaries_kernel(SummaryArgs a) {
 }  // namespace
 
 hipError_t launch_summaries(const SummaryArgs& a, hipStream_t s) {
-  const long long items = (long long)a.NBmax * a.Hkv * (kHeadDim / 8);
+  const long long blocks = a.prev_ctx_len ? (a.max_new < a.NBmax ? a.max_new : a.NBmax) : a.NBmax;
+  const long long items = blocks * a.Hkv * (kHeadDim / 8);
   const dim3 grid((unsigned)((items + 255) / 256), (unsigned)a.R);
   hipLaunchKernelGGL(summaries_kernel, grid, dim3(256), 0, s, a);
   return hipGetLastError();

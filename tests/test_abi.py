@@ -32,7 +32,8 @@ def lib():
 def test_header_declares_the_path():
     names = declared()
     for fn in ("oasis_score_blocks", "oasis_select_topk", "oasis_stage_blocks", "oasis_sparse_decode_attn",
-               "oasis_build_summaries", "oasis_attn_workspace_bytes", "oasis_last_error", "oasis_abi_version"):
+               "oasis_build_summaries", "oasis_update_summaries", "oasis_copy_blocks", "oasis_attn_workspace_bytes",
+               "oasis_pipeline_create", "oasis_pipeline_step", "oasis_last_error", "oasis_abi_version"):
         assert fn in names
 
 
@@ -81,6 +82,20 @@ def test_argument_checks_without_gpu(lib):
     z = lib.dims(0, 32, 8, 128, 16, 512)
     assert L.oasis_score_blocks(ctypes.byref(z), None, 5, 1, 4, None, None, None, None, None) == 0
     assert lib.oasis_last_error() == ""
+
+
+def test_growth_argument_checks_without_gpu(lib):
+    L = lib.lib()
+    d = lib.dims(2, 32, 8, 128, 16, 64)
+    assert L.oasis_update_summaries(ctypes.byref(d), None, 10, None, None, None, 0, None, None, None) == 1
+    assert "max_new_blocks" in lib.oasis_last_error()
+    assert L.oasis_update_summaries(ctypes.byref(d), None, 10, None, None, None, 1, None, None, None) == 1
+    assert "k_pages is NULL" in lib.oasis_last_error()
+    assert L.oasis_copy_blocks(ctypes.byref(d), None, None, 4, None, None, None, 4, None, None, None, 0, None) == 1
+    assert "max_blocks" in lib.oasis_last_error()
+    assert L.oasis_copy_blocks(ctypes.byref(d), None, None, 0, None, None, None, 4, None, None, None, 8, None) == 1
+    z = lib.dims(0, 32, 8, 128, 16, 64)                      # no requests: a no-op
+    assert L.oasis_copy_blocks(ctypes.byref(z), None, None, 4, None, None, None, 4, None, None, None, 8, None) == 0
 
 
 def test_pipeline_argument_checks_without_gpu(lib):

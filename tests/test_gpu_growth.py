@@ -159,3 +159,63 @@ def test_dense_to_sparse_transition():
     assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv)
     assert_attn_close(host_bits(st.out), ref_o)
     assert_lse_close(st.lse.cpu().numpy(), ref_l)
+
+
+def test_growing_layers_pipelined():
+    """The reasoning loop of §4.2.2 on the native issuer: several layers, one token appended per
+    step, each layer's compressed keys updated when a block completes, capped staging; every
+    layer's output and working set equal its own oracle chain."""
+    n_layers, steps, cap = 3, 40, 3
+    w = make_workload("c3", num_reqs=3, ctx_args=(100, 30, 400), steps=steps, budget=16 * 12, ar_queries=True)
+    c = w.cfg
+    B, H, K = c.block_size, c.num_kv_heads, c.K
+    hk_t, hv_t = pinned_pages(w)
+    hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
+    d = _dims(w)
+    bt = dev_i32(w.block_table)
+    path = DecodePath(d, c.T, K, hk_t, hv_t, bt, fetch_cap=cap)
+    layers = [LayerState(d, c.T, K) for _ in range(n_layers)]
+    qs = [w.layer_queries(l, steps) for l in range(n_layers)]
+    q_dev = [[dev_bf16(x) for x in qs[l]] for l in range(n_layers)]
+    ctx0 = w.ctx_len(0)
+    ctx_dev = [dev_i32(w.ctx_len(s)) for s in range(steps)]
+    ref = []
+    for l, st in enumerate(layers):
+        path.build_summaries(st, ctx_dev[0])
+        kmax, kmin = O.block_summaries(hk, w.block_table, ctx0, B, w.NBmax)
+        ref.append(dict(kmax=kmax, kmin=kmin, smap=np.full((c.num_reqs, H, K), -1, np.int32),
+                        stamp=np.zeros((c.num_reqs, H, K), np.int32),
+                        pk=np.zeros((c.num_reqs, K + 1, H, B, c.head_dim), np.uint16),
+                        pv=np.zeros((c.num_reqs, K + 1, H, B, c.head_dim), np.uint16)))
+    note("growing layers: issuing all steps")
+    for s in range(steps):
+        for l, st in enumerate(layers):
+            if s > 0:
+                P.oasis_update_summaries(d, hk_t, bt, ctx_dev[s - 1], ctx_dev[s], 1, st.kmax, st.kmin)
+            path.step_pipelined(st, q_dev[l][s], ctx_dev[s], s, growing=True)
+    path.join()
+    torch.cuda.synchronize()
+    none_sel = np.full((c.num_reqs, H, K), -1, np.int32)
+    zero_cnt = np.zeros((c.num_reqs, H), np.int32)
+    for l, st in enumerate(layers):
+        r_ = ref[l]
+        for s in range(steps):
+            ctx = w.ctx_len(s)
+            if s > 0:
+                O.update_summaries(hk, w.block_table, w.ctx_len(s - 1), ctx, B, r_["kmax"], r_["kmin"], 1)
+            O.stage_blocks(hk, hv, w.block_table, none_sel, zero_cnt, r_["smap"], r_["stamp"], s, r_["pk"], r_["pv"],
+                           ctx, B)
+            ref_o, ref_l = O.sparse_attend(qs[l][s], r_["pk"], r_["pv"], r_["smap"], ctx, B)
+            sc = O.block_scores(qs[l][s], r_["kmax"], r_["kmin"], ctx, H, B)
+            sel, cnt = O.select_topk(sc, ctx, K, B)
+            O.stage_blocks(hk, hv, w.block_table, sel, cnt, r_["smap"], r_["stamp"], s, r_["pk"], r_["pv"], ctx, B,
+                           copy_local=False, scores=sc, fetch_cap=cap)
+        assert not selection_diff(st.sel.cpu().numpy(), st.sel_count.cpu().numpy(), sel, cnt, sc)
+        assert np.array_equal(st.slot_map.cpu().numpy(), r_["smap"]), l
+        assert np.array_equal(st.slot_stamp.cpu().numpy(), r_["stamp"]), l
+        assert_attn_close(host_bits(st.out), ref_o, f"layer {l} out")
+        assert_lse_close(st.lse.cpu().numpy(), ref_l)
+        gmax = O.bf16_to_f64(host_bits(st.kmax))
+        ok = ~np.isnan(r_["kmax"])
+        assert np.array_equal(gmax[ok], r_["kmax"][ok])
+    path.close()

@@ -234,6 +234,19 @@ OASIS_API oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t
                                 int32_t copy_local, uint16_t* pool_k, uint16_t* pool_v, int32_t* moved,
                                 void* stream);
 
+/*
+ * Per-layer union of the per-head top-K sets (paper §4.4.1: for disaggregated
+ * admission the prefill node sends, per layer, every block whose token range
+ * at least one KV head selected, with its index). For every request r:
+ * union_ids[r][0..union_count[r]) = the distinct ids of sel[r][h][0..sel_count)
+ * over all heads h, ascending; union_ids[r][union_count[r]..Hkv*k) = -1. Ids
+ * outside [0, max_blocks) are ignored; counts are clamped to [0, k].
+ * union_ids: device [R][Hkv * k]; union_count: device [R]; sel, sel_count as
+ * produced by oasis_select_topk. max_blocks <= 524,288; 1 <= k <= 65536.
+ */
+OASIS_API oasis_status oasis_union_selection(const oasis_dims* dims, const int32_t* sel, const int32_t* sel_count,
+                                   int32_t k, int32_t* union_ids, int32_t* union_count, void* stream);
+
 /* Bytes of workspace oasis_sparse_decode_attn needs for these sizes (0 if invalid).
  * Calls that run at the same time need separate workspaces. */
 OASIS_API size_t oasis_attn_workspace_bytes(const oasis_dims* dims, int32_t num_q_tokens, int32_t k_slots);

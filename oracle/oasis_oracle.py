@@ -235,6 +235,26 @@ def select_topk(scores, ctx_len, k: int, block_size: int):
     return sel, cnt
 
 
+def union_selection(sel, sel_count):
+    """Per-layer union of the per-head top-K sets (paper §4.4.1, partial transfer).
+
+    For each request, the blocks whose token range at least one KV head
+    selected, in ascending block id. Returns (ids [R][Hkv*K], -1 padded;
+    count [R]).
+    """
+    R, H, K = sel.shape
+    ids = np.full((R, H * K), -1, np.int32)
+    cnt = np.zeros(R, np.int32)
+    for r in range(R):
+        u = set()
+        for h in range(H):
+            u.update(int(b) for b in sel[r, h, :sel_count[r, h]])
+        u = sorted(u)
+        ids[r, :len(u)] = u
+        cnt[r] = len(u)
+    return ids, cnt
+
+
 # ---------------------------------------------------------------------------
 # O3: delta selection + staging from the host tier
 # ---------------------------------------------------------------------------

@@ -24,7 +24,7 @@ EXPORTS = (
     "oasis_last_error", "oasis_abi_version", "oasis_build_summaries", "oasis_update_summaries",
     "oasis_copy_blocks", "oasis_score_blocks",
     "oasis_select_topk", "oasis_stage_blocks",
-    "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn",
+    "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn", "oasis_union_selection",
     "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_step", "oasis_pipeline_join",
     "oasis_pipeline_destroy", "oasis_pipeline_profile_begin", "oasis_pipeline_profile_end",
 )
@@ -90,6 +90,8 @@ def lib() -> ctypes.CDLL:
         L.oasis_stage_blocks.restype = _I32
         L.oasis_stage_blocks.argtypes = [_DIMS, _P, _P, _I64, _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
                                          _P, _P, _P, _P]
+        L.oasis_union_selection.restype = _I32
+        L.oasis_union_selection.argtypes = [_DIMS, _P, _P, _I32, _P, _P, _P]
         L.oasis_attn_workspace_bytes.restype = _SZ
         L.oasis_attn_workspace_bytes.argtypes = [_DIMS, _I32, _I32]
         L.oasis_sparse_decode_attn.restype = _I32
@@ -268,6 +270,17 @@ def oasis_stage_blocks(d: OasisDims, host_k, host_v, host_block_table, ctx_len, 
         _dev(slot_map, "slot_map", _I32T, nullable=True), _dev(slot_stamp, "slot_stamp", _I32T, nullable=True),
         int(step), int(fetch_cap), 1 if copy_local else 0, _dev(pool_k, "pool_k", _BF16),
         _dev(pool_v, "pool_v", _BF16), _dev(moved, "moved", _I32T, nullable=True), _stream(stream)))
+
+
+def oasis_union_selection(d: OasisDims, sel, sel_count, k: int, union_ids, union_count, stream=None) -> None:
+    R, H = d.num_reqs, d.num_kv_heads
+    _need(sel, R * H * k, "sel")
+    _need(sel_count, R * H, "sel_count")
+    _need(union_ids, R * H * k, "union_ids")
+    _need(union_count, R, "union_count")
+    _check("oasis_union_selection", lib().oasis_union_selection(
+        ctypes.byref(d), _dev(sel, "sel", _I32T), _dev(sel_count, "sel_count", _I32T), int(k),
+        _dev(union_ids, "union_ids", _I32T), _dev(union_count, "union_count", _I32T), _stream(stream)))
 
 
 def oasis_attn_workspace_bytes(d: OasisDims, num_q_tokens: int, k_slots: int) -> int:

@@ -369,6 +369,25 @@ oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, 
   return hip_status(oasis::launch_stage(a, static_cast<hipStream_t>(stream)), fn);
 }
 
+oasis_status oasis_union_selection(const oasis_dims* dims, const int32_t* sel, const int32_t* sel_count, int32_t k,
+                                   int32_t* union_ids, int32_t* union_count, void* stream) {
+  static const char* fn = "oasis_union_selection";
+  oasis_status st = oasis::check_dims(dims, fn);
+  if (st != OASIS_OK) return st;
+  if (k < 1 || k > 65536) return fail(OASIS_ERR_INVALID_ARG, "%s: k = %d outside [1, 65536]", fn, k);
+  if (dims->max_blocks > oasis::kUnionMaxBlocks)
+    return fail(OASIS_ERR_UNSUPPORTED, "%s: max_blocks %d > %d", fn, dims->max_blocks, oasis::kUnionMaxBlocks);
+  if ((long long)dims->num_kv_heads * k > (1LL << 30))
+    return fail(OASIS_ERR_UNSUPPORTED, "%s: num_kv_heads * k too large", fn);
+  if (dims->num_reqs == 0) return ok();
+  REQUIRE_PTR(sel, fn);
+  REQUIRE_PTR(sel_count, fn);
+  REQUIRE_PTR(union_ids, fn);
+  REQUIRE_PTR(union_count, fn);
+  oasis::UnionArgs a{sel, sel_count, union_ids, union_count, dims->num_reqs, dims->num_kv_heads, dims->max_blocks, k};
+  return hip_status(oasis::launch_union(a, static_cast<hipStream_t>(stream)), fn);
+}
+
 size_t oasis_attn_workspace_bytes(const oasis_dims* dims, int32_t num_q_tokens, int32_t k_slots) {
   if (oasis::check_dims(dims, "oasis_attn_workspace_bytes") != OASIS_OK || num_q_tokens < 1 || k_slots < 0)
     return 0;

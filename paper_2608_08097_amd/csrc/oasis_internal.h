@@ -90,6 +90,16 @@ struct CopyArgs {
 };
 hipError_t launch_copy_blocks(const CopyArgs& a, hipStream_t s);
 
+struct UnionArgs {
+  const int32_t* sel;       // [R][Hkv][k]
+  const int32_t* sel_count; // [R][Hkv]
+  int32_t* ids;             // [R][Hkv * k]
+  int32_t* count;           // [R]
+  int R, Hkv, NBmax, k;
+};
+constexpr int kUnionMaxBlocks = 1 << 19;  // LDS bitmap of 64 KiB (the default dynamic LDS limit)
+hipError_t launch_union(const UnionArgs& a, hipStream_t s);
+
 struct ScoreArgs {
   const uint16_t* q;
   const uint16_t* kmax;

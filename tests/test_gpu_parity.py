@@ -540,3 +540,36 @@ def test_abi_errors_on_device():
                              device="cuda"), ctx, smap, torch.zeros((1, 8), dtype=torch.int32, device="cuda"), None,
                              k, smap, smap.clone(), 0, k - 1, True, pool, pool, None)
     assert e.value.status == 1 and "scores" in str(e.value)  # a binding cap ranks misses by score
+
+
+# ---------------------------------------------------------------------------
+# per-layer union of the per-head sets (paper §4.4.1)
+# ---------------------------------------------------------------------------
+
+UNION_CASES = [
+    # (seed, R, H, NB, k)
+    (1, 4, 8, 8192, 128),
+    (2, 3, 8, 700, 1024),      # k above the candidates of some rows
+    (3, 2, 1, 33, 5),          # one head, a ragged bitmap word
+    (4, 5, 16, 100000, 64),    # many words per thread
+]
+
+
+@pytest.mark.parametrize("seed,R,H,NB,k", UNION_CASES)
+def test_union_selection_exact(seed, R, H, NB, k):
+    rng = np.random.default_rng(900 + seed)
+    n_cand = rng.integers(0, NB, size=R)
+    n_cand[0] = 0                                     # an empty request
+    sel, cnt = random_selection_h(910 + seed, n_cand, H, k)
+    if H > 1:
+        sel[-1, 1] = sel[-1, 0]                       # two heads with the same set
+        cnt[-1, 1] = cnt[-1, 0]
+    ref_ids, ref_cnt = O.union_selection(sel, cnt)
+    note(f"union seed={seed} R={R} H={H} NB={NB} k={k}")
+    d = P.dims(R, 8 * H, H, 128, 16, NB)
+    ids = torch.full((R, H * k), 77, dtype=torch.int32, device="cuda")
+    n = torch.full((R,), -5, dtype=torch.int32, device="cuda")
+    P.oasis_union_selection(d, dev_i32(sel), dev_i32(cnt), k, ids, n)
+    torch.cuda.synchronize()
+    assert np.array_equal(n.cpu().numpy(), ref_cnt)
+    assert np.array_equal(ids.cpu().numpy(), ref_ids)

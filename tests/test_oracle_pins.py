@@ -396,6 +396,26 @@ def test_stage_capped_converges():
                 assert sorted(smap[r, h]) == sorted(sel[r, h, :cnt[r, h]])
 
 
+def test_union_selection_against_numpy_and_properties():
+    """§4.4.1: a block is in the layer's set if at least one head selected it."""
+    rng = np.random.default_rng(17)
+    for trial in range(20):
+        R, H, K, NB = 3, int(rng.integers(1, 9)), int(rng.integers(1, 20)), int(rng.integers(1, 60))
+        sel = np.full((R, H, K), -1, np.int32)
+        cnt = rng.integers(0, min(K, NB) + 1, size=(R, H)).astype(np.int32)
+        for r in range(R):
+            for h in range(H):
+                sel[r, h, :cnt[r, h]] = np.sort(rng.choice(NB, size=cnt[r, h], replace=False))
+        ids, n = O.union_selection(sel, cnt)
+        for r in range(R):
+            ref = np.unique(np.concatenate([sel[r, h, :cnt[r, h]] for h in range(H)] + [np.zeros(0, np.int32)]))
+            assert n[r] == len(ref) and np.array_equal(ids[r, :n[r]], ref)
+            assert (ids[r, n[r]:] == -1).all()
+            assert max(cnt[r], default=0) <= n[r] <= cnt[r].sum()
+            for h in range(H):                         # every head's set is inside the union
+                assert set(sel[r, h, :cnt[r, h]]) <= set(ids[r, :n[r]])
+
+
 # ---------------------------------------------------------------------------
 # Growth of the context: summary updates and block copies between tiers
 # ---------------------------------------------------------------------------

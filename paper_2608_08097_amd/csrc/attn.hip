@@ -103,12 +103,15 @@ __device__ __forceinline__ void load_unit(UnitRegs& ur, int u, int ks, int local
 }
 
 // Zero the V values of tokens that are not attended (their probability is 0,
-// but 0 * NaN would poison the accumulator). Branch-free on purpose.
+// but 0 * NaN would poison the accumulator). Only lanes whose 8 tokens are not
+// all attended (a free slot, the tail of the local block) do any work; in a
+// full unit the whole wave skips it.
 template <int BS>
 __device__ __forceinline__ void mask_unit_v(UnitRegs& ur, int g) {
   const int cnt = BS == 16 ? (g < 2 ? ur.n0 : ur.n1) : ur.n0;
   const int t0 = BS == 16 ? (g & 1) * 8 : 8 * g;
   const int keep = cnt - t0;
+  if (keep >= 8) return;
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
 #pragma unroll

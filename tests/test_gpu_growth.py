@@ -215,7 +215,6 @@ def test_growing_layers_pipelined():
         assert np.array_equal(st.slot_stamp.cpu().numpy(), r_["stamp"]), l
         assert_attn_close(host_bits(st.out), ref_o, f"layer {l} out")
         assert_lse_close(st.lse.cpu().numpy(), ref_l)
-        gmax = O.bf16_to_f64(host_bits(st.kmax))
-        ok = ~np.isnan(r_["kmax"])
-        assert np.array_equal(gmax[ok], r_["kmax"][ok])
+        ok = ~np.isnan(r_["kmax"])                    # rows the oracle wrote; the rest was never initialised
+        assert np.array_equal(O.bf16_to_f64(host_bits(st.kmax)[ok]), r_["kmax"][ok])
     path.close()

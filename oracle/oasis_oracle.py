@@ -39,8 +39,8 @@ import math
 import numpy as np
 
 __all__ = [
-    "bf16_to_f64", "block_counts", "block_summaries", "block_scores",
-    "select_topk", "stage_blocks", "sparse_attend", "dense_attend",
+    "bf16_to_f64", "block_counts", "block_summaries", "update_summaries", "copy_blocks", "block_scores",
+    "select_topk", "union_selection", "stage_blocks", "sparse_attend", "dense_attend",
 ]
 
 

@@ -82,6 +82,8 @@ def parse():
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention comparison")
     ap.add_argument("--fetch-sweep", action="store_true",
                     help="step rate and bytes per step for fetch ratios 0.01 .. 0.2 and uncapped (Tab. eviction)")
+    ap.add_argument("--budget-sweep", action="store_true",
+                    help="step rate and attention for token budgets 1,024 / 2,048 / 4,096 against dense attention")
     ap.add_argument("--kernels-only", action="store_true",
                     help="only time the kernels alone on one stream (for hardware-counter passes)")
     ap.add_argument("--copy-calib", action="store_true",
@@ -102,6 +104,84 @@ def copy_calibration():
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_calibration_bytes": n, "dispatches": 3}), flush=True)
+
+
+def measured_peaks(torch, reps=10):
+    """Rates measured on this GPU for reference: a 1 GiB read (torch's row sums
+    over rows of 4,096 floats, its fastest read-only op here), a
+    1 GiB device-to-device copy (HBM read + write bytes per second) and a
+    256 MiB pinned host-to-device copy (the runtime's own copy path)."""
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    hsrc = torch.ones(256 << 20, dtype=torch.uint8, pin_memory=True)
+    hdst = torch.empty(hsrc.shape, dtype=torch.uint8, device="cuda")
+
+    def rate(fn, nbytes):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return nbytes * reps / (e0.elapsed_time(e1) * 1e6)
+
+    xf = src.view(torch.float32)
+    out = {"hbm_read_GBs": round(rate(lambda: xf.view(-1, 4096).sum(1), n), 1),
+           "hbm_copy_GBs": round(rate(lambda: dst.copy_(src), 2 * n), 1),
+           "h2d_memcpy_GBs": round(rate(lambda: hdst.copy_(hsrc, non_blocking=True), hsrc.numel()), 2),
+           "pcie_nominal_GBs": 64.0}
+    del src, dst, hsrc, hdst
+    torch.cuda.empty_cache()
+    return out
+
+
+def pctl(x):
+    """p10 / median / p90 of a sample, rounded."""
+    return [round(float(v), 2) for v in np.percentile(np.asarray(x, dtype=np.float64), [10, 50, 90])]
+
+
+def algorithmic_bytes(c, w, ctx, K):
+    """Algorithmic HBM bytes of one scorer launch and one attention call over all requests."""
+    n_cand = np.array([max(0, (int(L) + c.block_size - 1) // c.block_size - 1) for L in ctx])
+    bh = int(n_cand.sum()) * c.num_kv_heads                      # candidate block-heads per step
+    score_bytes = bh * (2 * c.head_dim * 2) + c.num_reqs * c.num_kv_heads * w.NBmax * 4 \
+        + c.num_reqs * c.T * c.num_q_heads * c.head_dim * 2
+    tok_per_head = np.minimum(K, n_cand) * c.block_size + np.array([L - c.block_size * nc
+                                                                    for L, nc in zip(ctx, n_cand)])
+    attn_bytes = int(tok_per_head.sum()) * c.num_kv_heads * (2 * c.head_dim * 2) \
+        + 2 * c.num_reqs * c.T * c.num_q_heads * c.head_dim * 2
+    return score_bytes, attn_bytes
+
+
+def cold_fill(torch, path, layers, ctx_d, c):
+    """Staging of a whole working set into empty slot maps (every selected block a miss, no cap):
+    the host-to-device gather at full size, back to back over the layer states."""
+    for st in layers:
+        st.reset()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for st in layers:
+        path.stage(st, ctx_d, 0, fetch_cap=path.k)
+    e1.record()
+    torch.cuda.synchronize()
+    us = 1000.0 * e0.elapsed_time(e1) / len(layers)
+    entries = sum(int(st.moved.sum().item()) for st in layers) / len(layers)
+    nbytes = entries * 2 * c.block_size * c.head_dim * 2
+    return {"avg_us": round(us, 1), "entries": round(entries, 1), "h2d_bytes": round(nbytes),
+            "h2d_GBs": round(nbytes / (us * 1e3), 2)}
+
+
+def describe(c, ctx, budget, K, fetch_cap, NL):
+    kinds = {"c1": "parity case", "c2": "batched serving", "c4": "long-context serving", "c5": "large-GQA stress"}
+    lens = f"{int(ctx[0])} tokens" if int(ctx.min()) == int(ctx.max()) else f"{int(ctx.min())}-{int(ctx.max())} tokens"
+    return (f"{c.name}: {kinds.get(c.name, c.name)}, {c.num_reqs} requests x {lens}, GQA "
+            f"{c.num_q_heads}q/{c.num_kv_heads}kv, head_dim {c.head_dim}, block {c.block_size}, "
+            f"{c.num_draft} draft tokens, budget {budget} (K={K}), fetch cap {fetch_cap} "
+            f"per KV head per step, AR(1) queries, {NL} rotating layer states")
 
 
 def cpu_baseline(w, hk, hv, queries, k, fetch_cap, budget_s):
@@ -208,10 +288,17 @@ def main():
         st.kmin.copy_(layers[0].kmin)
     qs = [[torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16) for x in w.layer_queries(l, per_layer_steps)]
           for l in range(NL)]
+    if args.budget_sweep:
+        path.close()
+        sweep = budget_sweep(P, torch, DecodePath, d, c, w, hk_t, hv_t, bt, layers, qs, ctx_d, ctx, args,
+                             (path.side, path.xfer))
+        dense = dense_attention(P, torch, w, hk_t, hv_t, ctx_d, d, c) if not args.no_dense else None
+        print(json.dumps({"budget_sweep": sweep, "dense_attention": dense}), flush=True)
+        return
     if args.fetch_sweep:
         path.close()
         print(json.dumps({"fetch_sweep": fetch_sweep(P, torch, DecodePath, d, c, K, hk_t, hv_t, bt, layers, qs,
-                                                     ctx_d, args)}), flush=True)
+                                                     ctx_d, args, (path.side, path.xfer))}), flush=True)
         return
     # The working set a layer holds when decoding starts: one uncapped fill from
     # its first prediction (untimed; decode steps are then capped).
@@ -256,15 +343,9 @@ def main():
         run(i, False)
     path.join()
     torch.cuda.synchronize()
-    us, n_prof = path.profile_end()
+    us, n_prof, per_step = path.profile_end(per_step=True)
     assert n_prof == args.steps
-    n_cand = np.array([max(0, (int(L) + c.block_size - 1) // c.block_size - 1) for L in ctx])
-    bh = int(n_cand.sum()) * c.num_kv_heads                      # candidate block-heads per step
-    score_bytes = bh * (2 * c.head_dim * 2) + c.num_reqs * c.num_kv_heads * w.NBmax * 4 \
-        + c.num_reqs * c.T * c.num_q_heads * c.head_dim * 2
-    tok_per_head = K * c.block_size + np.array([L - c.block_size * nc for L, nc in zip(ctx, n_cand)])
-    attn_bytes = int(tok_per_head.sum()) * c.num_kv_heads * (2 * c.head_dim * 2) \
-        + 2 * c.num_reqs * c.T * c.num_q_heads * c.head_dim * 2
+    score_bytes, attn_bytes = algorithmic_bytes(c, w, ctx, K)
     entry_bytes = 2 * c.block_size * c.head_dim * 2
     moved = moved_rate
     h2d_per_step = float(moved.sum()) / args.steps * entry_bytes
@@ -274,6 +355,13 @@ def main():
     iso = isolated(P, torch, path, layers, qs, ctx_d)
     score_gbs = score_bytes / (iso["score"] * 1e3)
     attn_gbs = attn_bytes / (iso["attn"] * 1e3)
+    # The same launches on one layer state only: its summaries and pools stay
+    # partly in the Infinity Cache (a warm reference, not the reported rate).
+    warm = isolated(P, torch, path, layers[:1], qs[:1], ctx_d)
+    path.join()
+    torch.cuda.synchronize()
+    cold = cold_fill(torch, path, layers, ctx_d, c)
+    peaks = measured_peaks(torch)
 
     dense = None
     if not args.no_dense and args.workload == "c4":
@@ -293,30 +381,35 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {
-            "workload": f"{c.name}: long-context serving, {c.num_reqs} requests x {int(ctx[0])} tokens, GQA "
-                        f"{c.num_q_heads}q/{c.num_kv_heads}kv, head_dim {c.head_dim}, block {c.block_size}, "
-                        f"{c.num_draft} draft tokens, budget {args.budget} (K={K}), fetch cap {fetch_cap} "
-                        f"per KV head per step, AR(1) queries, {NL} rotating layer states",
-            "global_batch": c.num_reqs, "seq_len": int(ctx[0]), "budget": args.budget,
+            "workload": describe(c, ctx, args.budget, K, fetch_cap, NL),
+            "global_batch": c.num_reqs, "seq_len": int(ctx.max()), "budget": args.budget,
             "fetch_ratio": args.fetch_ratio if fetch_cap < K else "all", "fetch_cap": fetch_cap,
             "parallelism": "single GPU",
         },
         "roofline": {
             "bound": "hbm", "kernel": "score_kernel (oasis_score_blocks)",
             "achieved": round(score_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(score_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
+            "frac": round(score_gbs / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic() if args.workload == "c4" else None,
             "algorithmic_bytes": score_bytes, "avg_us": round(iso["score"], 2),
             "timing": "64 back-to-back launches over the rotating layer states, one event pair",
         },
         "attention": {"avg_us": round(iso["attn"], 2), "algorithmic_bytes": attn_bytes,
-                      "achieved_GBs": round(attn_gbs, 1), "frac": round(attn_gbs / HBM_PEAK_GBS, 4)},
+                      "achieved_GBs": round(attn_gbs, 1), "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
+                      "frac_of_measured_read": round(attn_gbs / peaks["hbm_read_GBs"], 4)},
+        "score_frac_of_measured_read": round(score_gbs / peaks["hbm_read_GBs"], 4),
         "topk_us": round(iso["topk"], 2),
         "staging": {"avg_us_in_pipeline": round(us["stage"], 2), "h2d_bytes_per_step": round(h2d_per_step),
                     "entries_per_step": round(float(moved.sum()) / args.steps, 1),
-                    "h2d_GBs": round(h2d_per_step / (us["stage"] * 1e3), 2) if us["stage"] > 0 else None},
+                    "h2d_GBs": round(h2d_per_step / (us["stage"] * 1e3), 2) if us["stage"] > 0 else None,
+                    "cold_fill": cold,
+                    "cold_fill_frac_of_memcpy": round(cold["h2d_GBs"] / peaks["h2d_memcpy_GBs"], 4)},
+        "measured_peaks": peaks,
+        "warm_single_layer_us": {k_: round(v, 2) for k_, v in warm.items()},
         # region 2: dispatch-timed events per kernel inside the running pipeline; they include the
         # slowdown from concurrent kernels and host reads, and a few us of event latency each
         "pipeline_kernel_us": {k_: round(v, 2) for k_, v in us.items()},
+        "pipeline_kernel_p10_p50_p90_us": {k_: pctl(per_step[:, i]) for i, k_ in enumerate(P._lib.PROFILE_KINDS)},
         "dense_attention": dense,
     }
     if not args.no_cpu_baseline:
@@ -432,7 +525,51 @@ def run_reasoning(args, P, torch, DecodePath):
     print(json.dumps(result), flush=True)
 
 
-def fetch_sweep(P, torch, DecodePath, d, c, K, hk_t, hv_t, bt, layers, qs, ctx_d, args):
+def budget_sweep(P, torch, DecodePath, d, c, w, hk_t, hv_t, bt, layers, qs, ctx_d, ctx, args, streams):
+    """Token budgets 1,024 / 2,048 / 4,096 on the same inputs: for each, the step rate
+    (fetch cap = ratio x K), the attention alone over the working set, and the scorer."""
+    from paper_2608_08097_amd.path import LayerState
+    NL = len(layers)
+    out = []
+    for budget in (1024, 2048, 4096):
+        K = budget // c.block_size
+        cap = K if args.fetch_ratio >= 1.0 else max(1, int(math.floor(args.fetch_ratio * K)))
+        path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=cap,
+                          streams=streams)
+        sts = []
+        for l in range(NL):
+            st = LayerState(d, c.T, K)
+            st.kmax, st.kmin = layers[l].kmax, layers[l].kmin      # summaries are read-only here
+            path.predict(st, qs[l][0], ctx_d)
+            path.stage(st, ctx_d, 0, fetch_cap=K)
+            sts.append(st)
+        torch.cuda.synchronize()
+        for i in range(args.warmup):
+            path.step_pipelined(sts[i % NL], qs[i % NL][i // NL], ctx_d, i)
+        path.join()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.warmup, args.warmup + args.steps):
+            path.step_pipelined(sts[i % NL], qs[i % NL][i // NL], ctx_d, i)
+        path.join()
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        iso = isolated(P, torch, path, sts, qs, ctx_d)
+        path.close()
+        score_bytes, attn_bytes = algorithmic_bytes(c, w, ctx, K)
+        row = {"budget": budget, "K": K, "fetch_cap": cap, "steps_per_s": round(args.steps / el, 1),
+               "attn_us": round(iso["attn"], 2), "attn_bytes": attn_bytes,
+               "attn_GBs": round(attn_bytes / (iso["attn"] * 1e3), 1),
+               "score_us": round(iso["score"], 2), "score_GBs": round(score_bytes / (iso["score"] * 1e3), 1),
+               "topk_us": round(iso["topk"], 2)}
+        log(f"budget sweep {row}")
+        out.append(row)
+        del sts
+        torch.cuda.empty_cache()
+    return out
+
+
+def fetch_sweep(P, torch, DecodePath, d, c, K, hk_t, hv_t, bt, layers, qs, ctx_d, args, streams):
     """The fetch-cap ablation of §5.5.1 on this workload: for each ratio, the same
     steps from the same initial fill; entries and bytes moved per step, the step
     rate, and the host-to-device rate the staging sustains at that step rate."""
@@ -441,7 +578,8 @@ def fetch_sweep(P, torch, DecodePath, d, c, K, hk_t, hv_t, bt, layers, qs, ctx_d
     out = []
     for ratio in (0.01, 0.02, 0.05, 0.10, 0.20, 1.0):
         cap = K if ratio >= 1.0 else max(1, int(math.floor(ratio * K)))
-        path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=cap)
+        path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=cap,
+                          streams=streams)
         for l, st in enumerate(layers):
             st.reset()
             path.predict(st, qs[l][0], ctx_d)

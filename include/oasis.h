@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define OASIS_ABI_VERSION 2
+#define OASIS_ABI_VERSION 3
 
 /* Only the entry points below are exported from liboasis.so. */
 #if defined(__GNUC__) || defined(__clang__)
@@ -355,9 +355,13 @@ OASIS_API oasis_status oasis_pipeline_join(oasis_pipeline* pipeline, void* strea
 OASIS_API oasis_status oasis_pipeline_profile_begin(oasis_pipeline* pipeline, int32_t max_steps);
 
 /* Wait for the profiled steps and write the mean duration in microseconds of
- * attention, scoring, top-K and staging to avg_us[0..3] (steps: how many steps
- * were profiled, nullable); releases the profile's events. */
-OASIS_API oasis_status oasis_pipeline_profile_end(oasis_pipeline* pipeline, float* avg_us, int32_t* steps);
+ * attention, scoring, top-K and staging to avg_us[0..3]. step_us (nullable,
+ * caller-owned, room for max_steps x 4 floats as passed to profile_begin)
+ * receives each profiled step's four durations, step-major in the same order;
+ * steps (nullable) receives how many steps were profiled. Releases the
+ * profile's events. */
+OASIS_API oasis_status oasis_pipeline_profile_end(oasis_pipeline* pipeline, float* avg_us, float* step_us,
+                                                  int32_t* steps);
 
 /* Synchronize the device, then release the counters (and owned streams). NULL is a no-op. */
 OASIS_API void oasis_pipeline_destroy(oasis_pipeline* pipeline);

@@ -57,6 +57,7 @@ def dims(num_reqs, num_q_heads, num_kv_heads, head_dim, block_size, max_blocks) 
 
 
 _lib = None
+ABI_VERSION = 3  # OASIS_ABI_VERSION of include/oasis.h
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -77,6 +78,9 @@ def lib() -> ctypes.CDLL:
         L.oasis_last_error.argtypes = []
         L.oasis_abi_version.restype = _I32
         L.oasis_abi_version.argtypes = []
+        if L.oasis_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI version {L.oasis_abi_version()}, this binding expects "
+                               f"{ABI_VERSION}: rebuild it")
         L.oasis_build_summaries.restype = _I32
         L.oasis_build_summaries.argtypes = [_DIMS, _P, _I64, _P, _P, _P, _P, _P]
         L.oasis_update_summaries.restype = _I32
@@ -111,7 +115,8 @@ def lib() -> ctypes.CDLL:
         L.oasis_pipeline_profile_begin.restype = _I32
         L.oasis_pipeline_profile_begin.argtypes = [_P, _I32]
         L.oasis_pipeline_profile_end.restype = _I32
-        L.oasis_pipeline_profile_end.argtypes = [_P, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(_I32)]
+        L.oasis_pipeline_profile_end.argtypes = [_P, ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_float),
+                                                   ctypes.POINTER(_I32)]
         _lib = L
     return _lib
 
@@ -379,13 +384,24 @@ def oasis_pipeline_destroy(handle: int | None) -> None:
 PROFILE_KINDS = ("attn", "score", "topk", "stage")
 
 
+_PROF_CAP: dict[int, int] = {}
+
+
 def oasis_pipeline_profile_begin(handle: int, max_steps: int) -> None:
     _check("oasis_pipeline_profile_begin", lib().oasis_pipeline_profile_begin(handle, int(max_steps)))
+    _PROF_CAP[handle] = int(max_steps)
 
 
-def oasis_pipeline_profile_end(handle: int) -> tuple[dict[str, float], int]:
-    """Mean kernel durations (us) over the profiled steps, and the number of steps."""
+def oasis_pipeline_profile_end(handle: int, per_step: bool = False):
+    """Mean kernel durations (us) over the profiled steps and the number of steps; with
+    ``per_step`` also a [steps, 4] array of each step's durations (columns: PROFILE_KINDS)."""
     avg = (ctypes.c_float * 4)()
     n = _I32()
-    _check("oasis_pipeline_profile_end", lib().oasis_pipeline_profile_end(handle, avg, ctypes.byref(n)))
-    return {k: float(avg[i]) for i, k in enumerate(PROFILE_KINDS)}, int(n.value)
+    cap = _PROF_CAP.pop(handle, 0)
+    steps = (ctypes.c_float * (4 * max(cap, 1)))() if per_step else None
+    _check("oasis_pipeline_profile_end", lib().oasis_pipeline_profile_end(handle, avg, steps, ctypes.byref(n)))
+    means = {k: float(avg[i]) for i, k in enumerate(PROFILE_KINDS)}
+    if not per_step:
+        return means, int(n.value)
+    import numpy as np
+    return means, int(n.value), np.ctypeslib.as_array(steps)[: 4 * int(n.value)].reshape(-1, 4).copy()

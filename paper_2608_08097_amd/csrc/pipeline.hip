@@ -306,7 +306,7 @@ oasis_status oasis_pipeline_profile_begin(oasis_pipeline* p, int32_t max_steps) 
   return ok();
 }
 
-oasis_status oasis_pipeline_profile_end(oasis_pipeline* p, float* avg_us, int32_t* steps) {
+oasis_status oasis_pipeline_profile_end(oasis_pipeline* p, float* avg_us, float* step_us, int32_t* steps) {
   static const char* fn = "oasis_pipeline_profile_end";
   if (!p) return fail(OASIS_ERR_INVALID_ARG, "%s: pipeline is NULL", fn);
   if (!avg_us) return fail(OASIS_ERR_INVALID_ARG, "%s: avg_us is NULL", fn);
@@ -321,6 +321,7 @@ oasis_status oasis_pipeline_profile_end(oasis_pipeline* p, float* avg_us, int32_
       float ms = 0.f;
       if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
       sum[kind] += ms;
+      if (step_us) step_us[i * kProfKinds + kind] = 1000.f * ms;
     }
   }
   drop_profile(p);

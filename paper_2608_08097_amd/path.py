@@ -91,7 +91,7 @@ class DecodePath:
     def __init__(self, d: L.OasisDims, num_q_tokens: int, k: int, host_k: torch.Tensor, host_v: torch.Tensor,
                  block_table: torch.Tensor, first_draft: int = 1, num_draft: int | None = None,
                  scale: float | None = None, fetch_cap: int | None = None, native: bool = True,
-                 max_layers: int = 256):
+                 max_layers: int = 256, streams: tuple | None = None):
         self.dims, self.T, self.k = d, int(num_q_tokens), int(k)
         # step_pipelined issues through the library's native step issuer unless a timer is given
         self.native = bool(native)
@@ -104,9 +104,10 @@ class DecodePath:
         self.num_draft = int(num_draft if num_draft is not None else self.T - self.first_draft)
         self.host_k, self.host_v, self.block_table = host_k, host_v, block_table
         self.scale = scale if scale is not None else 1.0 / math.sqrt(d.head_dim)
-        # background streams (default priority): top-K prediction, KV transfer
-        self.side = torch.cuda.Stream()
-        self.xfer = torch.cuda.Stream()
+        # background streams (default priority): top-K prediction, KV transfer; paths
+        # created one after another can pass the same pair, which keeps the streams
+        # on the hardware queues they were first given
+        self.side, self.xfer = streams if streams is not None else (torch.cuda.Stream(), torch.cuda.Stream())
 
     def new_layer(self) -> LayerState:
         return LayerState(self.dims, self.T, self.k, self.block_table.device)
@@ -135,9 +136,10 @@ class DecodePath:
             raise RuntimeError("no native step has been issued yet")
         L.oasis_pipeline_profile_begin(self._pipe, max_steps)
 
-    def profile_end(self) -> tuple[dict[str, float], int]:
-        """Mean durations (us) of attention, scoring, top-K and staging, and the step count."""
-        return L.oasis_pipeline_profile_end(self._pipe)
+    def profile_end(self, per_step: bool = False):
+        """Mean durations (us) of attention, scoring, top-K and staging, and the step count
+        (with ``per_step``, also each step's four durations as a [steps, 4] array)."""
+        return L.oasis_pipeline_profile_end(self._pipe, per_step)
 
     def close(self):
         """Wait for the background streams and release the native issuer."""

@@ -471,9 +471,10 @@ def test_pipeline_profile():
         path.step_pipelined(st, qs[s], ctx_d, s)
     path.join()
     torch.cuda.synchronize()
-    us, n = path.profile_end()
-    assert n == 3
+    us, n, per_step = path.profile_end(per_step=True)
+    assert n == 3 and per_step.shape == (3, 4)
     assert all(0.0 < us[k_] < 1e5 for k_ in ("attn", "score", "topk", "stage")), us
+    np.testing.assert_allclose(per_step.mean(axis=0), [us[k_] for k_ in P._lib.PROFILE_KINDS], rtol=1e-4)
     with pytest.raises(P.OasisError):
         path.profile_end()
     path.close()

@@ -43,6 +43,10 @@ CASES = {
     "d1": lambda: make_workload("c1", num_draft=1, ctx_args=(2500,), budget=256),
     # one KV head group with 2 query heads, D = 2
     "g2": lambda: make_workload("c2", num_reqs=3, num_q_heads=16, num_draft=2, ctx_args=(700, 2200), budget=320),
+    # G = 4, D = 6: 24 scoring rows (two row tiles), 28 attention rows
+    "g4_d6": lambda: make_workload("c2", num_reqs=2, num_draft=6, ctx_args=(900, 2600), budget=384),
+    # G = 8, D = 6, B = 32: 48 scoring rows (three row tiles), 56 attention rows (four tiles)
+    "g8_d6_b32": lambda: make_workload("c5", num_reqs=2, num_draft=6, ctx_args=(2000,), budget=512),
 }
 
 
@@ -254,6 +258,8 @@ ATTN_CASES = [
     (6, 2, 32, 8, 5, 16, 16, [0, 300], 1.0),             # empty context; all slots free
     (7, 1, 40, 8, 4, 16, 300, [8192], 0.1),              # G = 5: 20 rows, many splits
     (8, 2, 16, 2, 5, 32, 33, [1000, 64], 0.25),
+    (9, 2, 64, 8, 7, 16, 50, [4000, 777], 0.2),          # 56 rows: four row tiles
+    (10, 2, 48, 8, 6, 32, 20, [3000, 100], 0.3),         # G = 6: 36 rows, three row tiles, B = 32
 ]
 
 

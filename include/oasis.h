@@ -287,7 +287,10 @@ OASIS_API oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const ui
  *   transfer stream: once the prediction is ready and this step's attention
  *     has read the pools, oasis_stage_blocks (delta selection with the fetch
  *     cap, then the gather; the paper's selection and transfer stages are one
- *     kernel here), with copy_local = !growing.
+ *     kernel here), with copy_local = 0. The local block is rewritten on
+ *     the foreground when `growing`; otherwise the context has not changed
+ *     since the local block was last staged (the caller stages it once, e.g.
+ *     in the initial fill) and it stays in place.
  * Consecutive calls for different layers overlap one layer's transfer with
  * the next layers' attention and prediction. The streams are ordered through
  * monotone counters in device memory (stream write-value after the producer,

@@ -238,7 +238,7 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   if ((st = oasis::make_topk_args(d, b.scores, ctx_len, p->k, b.sel, b.sel_count, &ta, fn)) != OASIS_OK) return st;
   if ((st = oasis::make_stage_args(d, p->host_k, p->host_v, p->num_pages, p->block_table, ctx_len, b.sel,
                                    b.sel_count, b.scores, p->k, b.slot_map, b.slot_stamp, step, p->fetch_cap,
-                                   growing ? 0 : 1, b.pool_k, b.pool_v, moved ? moved : b.moved, &ga, fn)) != OASIS_OK)
+                                   0, b.pool_k, b.pool_v, moved ? moved : b.moved, &ga, fn)) != OASIS_OK)
     return st;
   if (growing &&
       (st = oasis::make_stage_args(d, p->host_k, p->host_v, p->num_pages, p->block_table, ctx_len, nullptr, nullptr,

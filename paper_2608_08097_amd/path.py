@@ -203,7 +203,8 @@ class DecodePath:
         attention and prediction.
         With ``growing`` (one token appended per step) the local block is
         rewritten on the foreground before the attention, since it changes
-        every step; otherwise the transfer refreshes it.
+        every step; otherwise it is unchanged since it was last staged (the
+        initial fill stages it) and nothing moves it.
         ``timer`` records HIP events around each call on its own stream;
         ``moved`` (int32 [R][Hkv]) receives the entries this step copies.
         Without a timer the step goes through the library's native issuer (one
@@ -244,7 +245,7 @@ class DecodePath:
         xfer.wait_event(ev_attn)  # the gather overwrites slots the attention reads
         e = tm.begin("stage", xfer)
         L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, st.sel, st.sel_count,
-                             st.scores, self.k, st.slot_map, st.slot_stamp, step, self.fetch_cap, not growing,
+                             st.scores, self.k, st.slot_map, st.slot_stamp, step, self.fetch_cap, False,
                              st.pool_k, st.pool_v, st.moved if moved is None else moved, xfer)
         tm.end("stage", xfer, e)
         ev_staged = torch.cuda.Event()

@@ -166,7 +166,9 @@ OASIS_API oasis_status oasis_copy_blocks(const oasis_dims* dims, const uint16_t*
  * b in [n_cand_r, NBmax) are -inf. No 1/sqrt(d) factor (ranking only).
  *
  * Requires kmin <= kmax coordinate-wise (as built by oasis_build_summaries).
- * Arithmetic: bf16 products, fp32 accumulation (MFMA). num_draft * G <= 64.
+ * Arithmetic: bf16 products, fp32 accumulation (MFMA for 5 to 64 rows; up to
+ * 4 rows, a quarter of an MFMA tile, v_dot2 on the vector ALUs).
+ * num_draft * G <= 64.
  * All pointers are device pointers.
  */
 OASIS_API oasis_status oasis_score_blocks(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens,

@@ -109,6 +109,20 @@ struct ScoreArgs {
   int R, Hq, Hkv, G, T, first_draft, num_draft, B, NBmax;
 };
 hipError_t launch_score(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t = {});
+// Scorer on the vector ALUs for at most kScoreValuMaxRows rows (launch_score
+// calls it for those row counts).
+constexpr int kScoreValuMaxRows = 4;
+hipError_t launch_score_valu(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t = {});
+
+// Split bf16 pairs into their non-negative and non-positive parts (bitwise, exact).
+__device__ __forceinline__ void split_sign(u32x4 v, u32x4& pos, u32x4& neg) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const uint32_t negmask = ((v[w] & 0x80008000u) >> 15) * 0xFFFFu;
+    neg[w] = v[w] & negmask;
+    pos[w] = v[w] & ~negmask;
+  }
+}
 
 struct TopkArgs {
   const float* scores;

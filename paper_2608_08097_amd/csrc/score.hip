@@ -5,10 +5,11 @@
 // For one row q and a block with per-coordinate bounds kmin <= kmax,
 //   sum_d max(q_d kmin_d, q_d kmax_d) = sum_d (q+_d kmax_d + q-_d kmin_d)
 // with q+ = max(q, 0), q- = min(q, 0): exactly a dot product of [q+ | q-]
-// (2d bf16 values, exact) with [kmax ; kmin]. The rows of one KV head (up to
-// 64) times a tile of 16 blocks is therefore a dense [rows x 256] x [256 x 16]
-// product, done with v_mfma_f32_16x16x32_bf16 (fp32 accumulation), and the
-// row maximum is taken in the epilogue with two cross-lane exchanges.
+// (2d bf16 values, exact) with [kmax ; kmin]. The rows of one KV head (5 to
+// 64 here; fewer go to the vector-ALU scorer of score_valu.hip) times a tile
+// of 16 blocks is therefore a dense [rows x 256] x [256 x 16] product, done
+// with v_mfma_f32_16x16x32_bf16 (fp32 accumulation), and the row maximum is
+// taken in the epilogue with two cross-lane exchanges.
 //
 // Memory: every summary byte is read once. A wave owns TPW consecutive tiles
 // of 16 blocks; for a tile, lane (g, n) loads 16 bytes of block n at byte
@@ -20,16 +21,6 @@
 namespace oasis {
 
 namespace {
-
-// Split bf16 pairs into their non-negative and non-positive parts (bitwise, exact).
-__device__ __forceinline__ void split_sign(u32x4 v, u32x4& pos, u32x4& neg) {
-#pragma unroll
-  for (int w = 0; w < 4; ++w) {
-    const uint32_t negmask = ((v[w] & 0x80008000u) >> 15) * 0xFFFFu;
-    neg[w] = v[w] & negmask;
-    pos[w] = v[w] & ~negmask;
-  }
-}
 
 template <int NRT, int TPW>
 __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
@@ -123,6 +114,8 @@ hipError_t launch_t(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t) {
 
 hipError_t launch_score(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t) {
   const int rows = a.num_draft * a.G;
+  // a quarter of a 16-row tile or less: no MFMA
+  if (rows <= kScoreValuMaxRows) return launch_score_valu(a, s, t);
   switch ((rows + 15) / 16) {
     case 1: return launch_t<1, 4>(a, s, t);
     case 2: return launch_t<2, 4>(a, s, t);

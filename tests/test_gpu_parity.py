@@ -39,7 +39,7 @@ CASES = {
     "c1": lambda: make_workload("c1"),
     # B = 32, 64 scoring rows (G = 8, D = 8), 72 attention rows
     "gqa8_b32": lambda: make_workload("c5", num_reqs=2, ctx_args=(3000,), budget=1024),
-    # G = 4, D = 1: 4 scoring rows (padded tile), 8 attention rows
+    # G = 4, D = 1: 4 scoring rows (vector-ALU scorer), 8 attention rows
     "d1": lambda: make_workload("c1", num_draft=1, ctx_args=(2500,), budget=256),
     # one KV head group with 2 query heads, D = 2
     "g2": lambda: make_workload("c2", num_reqs=3, num_q_heads=16, num_draft=2, ctx_args=(700, 2200), budget=320),
@@ -106,6 +106,42 @@ def test_scores(case):
 # ---------------------------------------------------------------------------
 # a2 selection on given scores: bit-exact
 # ---------------------------------------------------------------------------
+
+SCORE_ROW_CASES = [
+    # (seed, R, Hq, Hkv, T, first_draft, num_draft, NBmax, B, ctx lengths): rows = G * num_draft
+    (1, 2, 8, 8, 2, 1, 1, 300, 16, [4800, 1000]),          # 1 row (vector-ALU scorer)
+    (2, 2, 16, 8, 2, 1, 1, 130, 16, [2080, 17]),           # 2 rows
+    (3, 3, 8, 8, 4, 1, 3, 200, 32, [6400, 33, 0]),         # 3 rows, B = 32, an empty context
+    (10, 2, 32, 8, 2, 1, 1, 333, 16, [5328, 700]),         # 4 rows: the largest vector-ALU case
+    (4, 2, 40, 8, 2, 1, 1, 257, 16, [4112, 4000]),         # 5 rows (G = 5): the smallest MFMA case
+    (5, 2, 32, 8, 3, 0, 2, 129, 16, [2064, 1500]),         # 8 rows, the verify row scoring too
+    (6, 2, 24, 8, 4, 1, 3, 300, 16, [4800, 2222]),         # 9 rows
+    (7, 1, 17, 1, 2, 1, 1, 1000, 16, [16000]),             # 17 rows: two row tiles
+    (8, 2, 64, 8, 6, 1, 5, 150, 32, [4800, 1234]),         # 40 rows: three row tiles
+    (9, 1, 64, 8, 9, 1, 8, 64, 32, [2048]),                # 64 rows: four row tiles
+]
+
+
+@pytest.mark.parametrize("seed,R,Hq,Hkv,T,first_draft,num_draft,NB,B,lens", SCORE_ROW_CASES)
+def test_scores_rows(seed, R, Hq, Hkv, T, first_draft, num_draft, NB, B, lens):
+    """Every scorer variant (vector ALUs up to 4 rows, MFMA with 1 to 4 row tiles) against the oracle."""
+    d_head = 128
+    q = random_bf16(500 + seed, (R, T, Hq, d_head))
+    a = random_bf16(510 + seed, (R, Hkv, NB, d_head))
+    b = random_bf16(520 + seed, (R, Hkv, NB, d_head), scale=2.0)
+    av, bv = O.bf16_to_f64(a), O.bf16_to_f64(b)
+    kmax_bits = np.where(av >= bv, a, b)
+    kmin_bits = np.where(av >= bv, b, a)
+    ctx = np.array(lens, np.int32)
+    ref = O.block_scores(q, O.bf16_to_f64(kmax_bits), O.bf16_to_f64(kmin_bits), ctx, Hkv, B, first_draft, num_draft)
+    note(f"scores rows={Hq // Hkv * num_draft} seed={seed}")
+    d = P.dims(R, Hq, Hkv, d_head, B, NB)
+    scores = torch.full((R, Hkv, NB), 7.0, device="cuda")
+    P.oasis_score_blocks(d, dev_bf16(q), T, first_draft, num_draft, dev_bf16(kmax_bits), dev_bf16(kmin_bits),
+                         dev_i32(ctx), scores)
+    torch.cuda.synchronize()
+    assert_scores_close(scores.cpu().numpy(), ref)
+
 
 SELECT_CASES = [
     # (seed, R, H, NBmax, B, ctx lengths, k, n_distinct)

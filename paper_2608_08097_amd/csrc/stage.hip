@@ -10,9 +10,8 @@
 // the selected block-head entries from pinned host memory over PCIe and
 // writes them into the resident GPU pages.
 //
-// A fixed grid of up to kCopyWorkgroups 256-thread workgroups walks the
-// (request, KV head) pairs (workgroup w takes pairs w, w + grid, ...); for each
-// pair it does:
+// A grid of 256-thread workgroups walks the (request, KV head) pairs
+// (workgroup w takes pairs w, w + grid, ...); for each pair it does:
 //   plan   the slot map, stamps and selection sit in LDS; misses and stale
 //          slots are compacted by workgroup scans and ranked one item per
 //          thread (misses by score under a cap, stale slots by (stamp, slot));
@@ -22,14 +21,20 @@
 //          whole batch (PF x 2 x B x d x 2 bytes) are issued before any is
 //          stored, K goes to the pool token-major, V is transposed through LDS
 //          into the d x B layout the attention kernel reads.
-// Host reads take microseconds to return, so the plans run one pair per
-// workgroup in parallel and each workgroup keeps a batch of entries in flight.
-// Host reads beyond what saturates the link only queue inside the GPU, where
-// they slow the HBM traffic of concurrent kernels: measured on MI355X with a
-// capped delta of 3 MB per step, 8 entries per workgroup in flight (3 MB)
-// stretch a concurrent block scan from 57 to 98 us, 2 entries (2 MB) to 88 us
-// at the same transfer time, and 1 entry on 32 workgroups to 77 us but with a
-// transfer 20 % slower; 64 workgroups x 2 entries gave the best step rate.
+// Host reads take microseconds to return, so the plans run in parallel and
+// each workgroup keeps a batch of entries in flight. Host reads beyond what
+// saturates the link only queue inside the GPU, where they slow the HBM
+// traffic of concurrent kernels (measured on MI355X: with 3 MB moved per step,
+// 8 entries per workgroup in flight on 64 workgroups stretch a concurrent
+// block scan from 57 to 98 us, 2 entries to 88 us). The grid is therefore one
+// workgroup per two pairs, kept between kCopyWorkgroupsMin and
+// kCopyWorkgroupsMax, with 2 entries in flight per workgroup (more on small
+// grids, so that the link still fills). Measured step rates (steps/s) for
+// 32 / 48 / 64 workgroups: 8 x 131,072 tokens (64 pairs) 10,490 / 9,790 /
+// 9,290; 32 requests of 16K-32K tokens (256 pairs) 7,920 / 8,540 / 8,400;
+// 16 x 65,536 tokens with B = 32 (128 pairs) 3,510 / 3,510 / 3,700. Fewer
+// workgroups mean more plans in series per workgroup, which the last two
+// cannot afford.
 #include <climits>
 
 #include "oasis_internal.h"
@@ -42,8 +47,9 @@ constexpr int kPlanThreads = 256;
 constexpr int kMaxK = 1024;
 constexpr int kPer = kMaxK / kPlanThreads;  // items per thread in the scans
 constexpr int kKeyPad = 4;
-constexpr int kCopyWorkgroups = 64;
-constexpr int kCopyInflight = 128;  // block-head entries (K and V) in flight over the whole grid
+constexpr int kCopyWorkgroupsMin = 32;
+constexpr int kCopyWorkgroupsMax = 64;
+constexpr int kCopyInflightMin = 64;  // block-head entries (K and V) in flight over the whole grid, at least
 
 // Monotone map of a float onto uint32 (larger float, larger key; -0 and +0 equal).
 __device__ inline unsigned order_key(float f) {
@@ -88,15 +94,36 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
   __shared__ __align__(16) unsigned s_mkey[kMaxK + kKeyPad];
   __shared__ __align__(16) int s_skey[kMaxK + kKeyPad];
   __shared__ int s_midx[kMaxK], s_madm[kMaxK], s_sslot[kMaxK];
+  // by selection index: the page of the block and its score key (under a possible cap)
+  __shared__ int s_selpage[kMaxK];
+  __shared__ unsigned s_selkey[kMaxK];
 
   const long long base = (long long)rh * k;
   int m = a.sel_count[rh];
   m = m < 0 ? 0 : (m > k ? k : m);
-  for (int i = tid; i < k; i += kPlanThreads) {
-    s_sel[i] = i < m ? a.sel[base + i] : INT_MAX;
-    s_hit[i] = 0;
-    s_map[i] = a.slot_map[base + i];
-    s_stamp[i] = a.slot_stamp[base + i];
+  // The page of every selected block (and, when a cap may bind, its score) is
+  // fetched as soon as the block id arrives, so that these dependent loads
+  // overlap the search below instead of stalling the pairing later.
+  const bool may_cap = a.fetch_cap < m;
+  int pg[kPer];
+  unsigned ky[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int i = tid + j * kPlanThreads;
+    pg[j] = -1;
+    ky[j] = 0u;
+    if (i < k) {
+      const int b = i < m ? a.sel[base + i] : INT_MAX;
+      s_sel[i] = b;
+      s_hit[i] = 0;
+      s_map[i] = a.slot_map[base + i];
+      s_stamp[i] = a.slot_stamp[base + i];
+      if (i < m) {
+        const bool in_row = b >= 0 && b < a.NBmax;
+        if (in_row) pg[j] = a.block_table[(long long)r * a.NBmax + b];
+        if (may_cap) ky[j] = order_key(in_row ? a.scores[(long long)rh * a.NBmax + b] : -__builtin_inff());
+      }
+    }
   }
   __syncthreads();
 
@@ -116,6 +143,14 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
       }
     }
     s_keep[s] = keep;
+  }
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int i = tid + j * kPlanThreads;
+    if (i < k) {
+      s_selpage[i] = pg[j];
+      s_selkey[i] = ky[j];
+    }
   }
   __syncthreads();
 
@@ -149,12 +184,7 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
     for (int j = 0; j < kPer; ++j) {
       const int i = i0 + j;
       if (i < m && !s_hit[i]) {
-        unsigned key = 0;
-        if (capped) {
-          const int b = s_sel[i];
-          key = order_key((b >= 0 && b < a.NBmax) ? a.scores[(long long)rh * a.NBmax + b] : -__builtin_inff());
-        }
-        s_mkey[mr] = key;
+        s_mkey[mr] = capped ? s_selkey[i] : 0u;
         s_midx[mr] = i;
         ++mr;
       }
@@ -227,8 +257,7 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
       // a slot map holding one block twice can leave fewer victims than misses
       const int v = ar < n_vict ? s_vict[ar] : -1;
       const int blk = s_sel[s_midx[c]];
-      int page = -1;
-      if (v >= 0 && blk >= 0 && blk < a.NBmax) page = a.block_table[(long long)r * a.NBmax + blk];
+      int page = v >= 0 ? s_selpage[s_midx[c]] : -1;
       if (page < 0 || page >= a.num_pages) page = -1;
       s_slot[ar] = v;
       s_page[ar] = page;
@@ -338,8 +367,11 @@ __global__ __launch_bounds__(kPlanThreads) void stage_kernel(StageArgs a) {
 template <int BS>
 hipError_t launch_bs(const StageArgs& a, hipStream_t s, const LaunchTiming& t) {
   const int nrh = a.R * a.Hkv;
-  const int grid = nrh < kCopyWorkgroups ? nrh : kCopyWorkgroups;
-  const int pf = kCopyInflight / grid;  // entries per workgroup batch
+  if (nrh <= 0) return hipSuccess;
+  int grid = nrh / 2;
+  grid = grid < kCopyWorkgroupsMin ? kCopyWorkgroupsMin : (grid > kCopyWorkgroupsMax ? kCopyWorkgroupsMax : grid);
+  if (grid > nrh) grid = nrh;
+  const int pf = grid * 2 >= kCopyInflightMin ? 2 : kCopyInflightMin / grid;  // entries per workgroup batch
   if (pf >= 8)
     launch_kernel(stage_kernel<BS, 8>, dim3(grid), dim3(kPlanThreads), s, t, a);
   else if (pf >= 4)

@@ -428,7 +428,8 @@ def run_reasoning(args, P, torch, DecodePath):
     block is refreshed, and the pipelined step runs (attention on the
     foreground, prediction and capped staging behind it). The host K/V tier is
     shared by the layers; each layer has its own summaries, working set and
-    query stream. Queries follow the AR(1) recipe, drawn on the GPU from a
+    query stream. The active (local) blocks are device-resident, standing in for
+    the model's own KV writes, so only the delta transfer crosses PCIe. Queries follow the AR(1) recipe, drawn on the GPU from a
     seeded generator (2.7 G values would take a minute to draw on the host).
     Reports tokens/s, layer-steps/s, and T_pipe against Delta_prefetch =
     T_step / N_layer.
@@ -452,6 +453,16 @@ def run_reasoning(args, P, torch, DecodePath):
     ctx_d = [torch.from_numpy(w.ctx_len(s_)).cuda() for s_ in range(S)]
     path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=fetch_cap,
                       max_layers=NL)
+    # The blocks that are a request's local block during the run live in device
+    # pages, as a model writes its newest tokens on the GPU: the local refresh
+    # and the compressed-key update of a completed block read them there, and
+    # only the delta transfer reads the host tier.
+    lpages, ltable = w.local_block_pages(S)
+    lidx = torch.from_numpy(lpages)
+    dev_k = hk_t[lidx].cuda().view(torch.bfloat16)
+    dev_v = hv_t[lidx].cuda().view(torch.bfloat16)
+    dev_bt = torch.from_numpy(ltable).cuda()
+    path.set_local_source(dev_k, dev_v, dev_bt)
     layers = [path.new_layer() for _ in range(NL)]
     path.build_summaries(layers[0], ctx_d[0])
     gen = torch.Generator(device="cuda")
@@ -477,12 +488,14 @@ def run_reasoning(args, P, torch, DecodePath):
             path.stage(st, ctx_d[0], 0, fetch_cap=K)
         torch.cuda.synchronize()
 
+    moved_log = torch.zeros((S, NL, c.num_reqs, c.num_kv_heads), dtype=torch.int32, device="cuda")
+
     def decode():
         for s_ in range(S):
             for l, st in enumerate(layers):
                 if s_:
-                    P.oasis_update_summaries(d, path.host_k, bt, ctx_d[s_ - 1], ctx_d[s_], 1, st.kmax, st.kmin)
-                path.step_pipelined(st, qs[l][s_], ctx_d[s_], s_, growing=True)
+                    P.oasis_update_summaries(d, dev_k, dev_bt, ctx_d[s_ - 1], ctx_d[s_], 1, st.kmax, st.kmin)
+                path.step_pipelined(st, qs[l][s_], ctx_d[s_], s_, growing=True, moved=moved_log[s_, l])
         path.join()
         torch.cuda.synchronize()
 
@@ -493,6 +506,8 @@ def run_reasoning(args, P, torch, DecodePath):
     t0 = time.perf_counter()
     decode()
     elapsed = time.perf_counter() - t0
+    entries = float(moved_log.sum().item()) / (S * NL)   # per layer-step, this timed pass
+    entry_bytes = 2 * c.block_size * c.head_dim * 2
     # same pass again with per-kernel dispatch timing
     path.build_summaries(layers[0], ctx_d[0])
     prime()
@@ -516,6 +531,10 @@ def run_reasoning(args, P, torch, DecodePath):
         "prefetch_rate": {"delta_prefetch_us": round(delta, 2), "t_pred_us": round(prof["score"] + prof["topk"], 2),
                           "t_transfer_us": round(prof["stage"], 2), "t_pipe_us": round(t_pipe, 2),
                           "t_pipe_le_delta": bool(t_pipe <= delta)},
+        "staging": {"entries_per_layer_step": round(entries, 1),
+                    "h2d_bytes_per_layer_step": round(entries * entry_bytes),
+                    "h2d_GBs_in_transfer": round(entries * entry_bytes / (prof["stage"] * 1e3), 2),
+                    "h2d_GBs_at_step_rate": round(entries * entry_bytes * NL * S / elapsed / 1e9, 2)},
         "pipeline_kernel_us": {k_: round(v, 2) for k_, v in prof.items()},
     }
     path.close()

@@ -342,6 +342,19 @@ OASIS_API oasis_status oasis_pipeline_create(const oasis_dims* dims, int32_t num
 OASIS_API oasis_status oasis_pipeline_set_layer(oasis_pipeline* pipeline, int32_t layer,
                                       const oasis_layer_buffers* buffers);
 
+/* Pages the local block is refreshed from when a step is `growing` (by default
+ * the host tier given at create). A growing context's newest tokens are written
+ * by the model on the GPU, so a caller that keeps the active blocks in device
+ * pages passes them here and the refresh stays off the PCIe link. k_pages /
+ * v_pages: bf16 [num_pages][Hkv][B][d], device memory or pinned host memory
+ * (the library resolves the address); block_table: device [R][max_blocks],
+ * -1 or out-of-range ids skipped. All three NULL restores the host tier. The
+ * pointers stay the caller's and must outlive the steps that use them; steps
+ * already issued keep the source they were issued with. */
+OASIS_API oasis_status oasis_pipeline_set_local_source(oasis_pipeline* pipeline, const uint16_t* k_pages,
+                                             const uint16_t* v_pages, int64_t num_pages,
+                                             const int32_t* block_table);
+
 /* Issue one decode step of `layer` (see above). q: bf16 device [R][T][Hq][d];
  * ctx_len: device [R]; step: the stamp of this step's selection; moved: where
  * the transfer writes its per-(r, h) entry counts (NULL: the layer's buffer). */

@@ -25,7 +25,8 @@ EXPORTS = (
     "oasis_copy_blocks", "oasis_score_blocks",
     "oasis_select_topk", "oasis_stage_blocks",
     "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn", "oasis_union_selection",
-    "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_step", "oasis_pipeline_join",
+    "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_set_local_source", "oasis_pipeline_step",
+    "oasis_pipeline_join",
     "oasis_pipeline_destroy", "oasis_pipeline_profile_begin", "oasis_pipeline_profile_end",
 )
 
@@ -106,6 +107,8 @@ def lib() -> ctypes.CDLL:
                                             _I32, _P, _P, ctypes.POINTER(_P)]
         L.oasis_pipeline_set_layer.restype = _I32
         L.oasis_pipeline_set_layer.argtypes = [_P, _I32, ctypes.POINTER(OasisLayerBuffers)]
+        L.oasis_pipeline_set_local_source.restype = _I32
+        L.oasis_pipeline_set_local_source.argtypes = [_P, _P, _P, _I64, _P]
         L.oasis_pipeline_step.restype = _I32
         L.oasis_pipeline_step.argtypes = [_P, _I32, _P, _P, _I32, _I32, _P, _P]
         L.oasis_pipeline_join.restype = _I32
@@ -336,6 +339,22 @@ def oasis_pipeline_create(d: OasisDims, num_q_tokens: int, first_draft: int, num
     _PIPE_SIZES[h.value] = (d.num_reqs * int(num_q_tokens) * d.num_q_heads * d.head_dim, d.num_reqs,
                             d.num_reqs * d.num_kv_heads)
     return h.value
+
+
+def oasis_pipeline_set_local_source(handle: int, d: OasisDims, k_pages, v_pages, block_table) -> None:
+    """Pages a growing step refreshes the local block from (all None: the host tier)."""
+    if k_pages is None and v_pages is None and block_table is None:
+        _check("oasis_pipeline_set_local_source", lib().oasis_pipeline_set_local_source(handle, None, None, 0, None))
+        return
+    if k_pages is None or v_pages is None or block_table is None:
+        raise ValueError("k_pages, v_pages and block_table must all be given or all be None")
+    if k_pages.shape != v_pages.shape:
+        raise ValueError("k_pages and v_pages differ in shape")
+    _need(k_pages, k_pages.shape[0] * d.num_kv_heads * d.block_size * d.head_dim, "k_pages")
+    _need(block_table, d.num_reqs * d.max_blocks, "block_table")
+    _check("oasis_pipeline_set_local_source", lib().oasis_pipeline_set_local_source(
+        handle, _host_or_dev(k_pages, "k_pages", _BF16), _host_or_dev(v_pages, "v_pages", _BF16),
+        int(k_pages.shape[0]), _dev(block_table, "block_table", _I32T)))
 
 
 def oasis_pipeline_set_layer(handle: int, layer: int, d: OasisDims, num_q_tokens: int, k: int, kmax, kmin, scores,

@@ -33,6 +33,11 @@ struct oasis_pipeline {
   const uint16_t* host_v;
   int64_t num_pages;
   const int32_t* block_table;
+  // where a growing step refreshes the local block from (the host tier unless set)
+  const uint16_t* local_k;
+  const uint16_t* local_v;
+  int64_t local_num_pages;
+  const int32_t* local_block_table;
   int32_t max_layers;
   hipStream_t pred, xfer;
   bool own_streams;
@@ -175,6 +180,10 @@ oasis_status oasis_pipeline_create(const oasis_dims* dims, int32_t num_q_tokens,
   p->host_v = static_cast<const uint16_t*>(hv);
   p->num_pages = num_pages;
   p->block_table = host_block_table;
+  p->local_k = p->host_k;
+  p->local_v = p->host_v;
+  p->local_num_pages = num_pages;
+  p->local_block_table = host_block_table;
   p->max_layers = max_layers;
   p->layers = new (std::nothrow) oasis_layer_buffers[max_layers]();
   p->staged = new (std::nothrow) uint32_t[max_layers]();
@@ -201,6 +210,31 @@ oasis_status oasis_pipeline_create(const oasis_dims* dims, int32_t num_q_tokens,
     return hip_status(e, fn);
   }
   *pipeline = p;
+  return ok();
+}
+
+oasis_status oasis_pipeline_set_local_source(oasis_pipeline* p, const uint16_t* k_pages, const uint16_t* v_pages,
+                                             int64_t num_pages, const int32_t* block_table) {
+  static const char* fn = "oasis_pipeline_set_local_source";
+  if (!p) return fail(OASIS_ERR_INVALID_ARG, "%s: pipeline is NULL", fn);
+  if (!k_pages && !v_pages && !block_table) {  // back to the host tier
+    p->local_k = p->host_k;
+    p->local_v = p->host_v;
+    p->local_num_pages = p->num_pages;
+    p->local_block_table = p->block_table;
+    return ok();
+  }
+  if (!k_pages || !v_pages || !block_table)
+    return fail(OASIS_ERR_INVALID_ARG, "%s: k_pages, v_pages and block_table must all be set or all be NULL", fn);
+  if (num_pages < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: num_pages < 1", fn);
+  const void *kv = nullptr, *vv = nullptr;
+  oasis_status st;
+  if ((st = oasis::device_view(k_pages, &kv, "k_pages", fn)) != OASIS_OK) return st;
+  if ((st = oasis::device_view(v_pages, &vv, "v_pages", fn)) != OASIS_OK) return st;
+  p->local_k = static_cast<const uint16_t*>(kv);
+  p->local_v = static_cast<const uint16_t*>(vv);
+  p->local_num_pages = num_pages;
+  p->local_block_table = block_table;
   return ok();
 }
 
@@ -241,9 +275,9 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
                                    0, b.pool_k, b.pool_v, moved ? moved : b.moved, &ga, fn)) != OASIS_OK)
     return st;
   if (growing &&
-      (st = oasis::make_stage_args(d, p->host_k, p->host_v, p->num_pages, p->block_table, ctx_len, nullptr, nullptr,
-                                   nullptr, p->k, nullptr, nullptr, 0, p->k, 1, b.pool_k, b.pool_v, nullptr, &la,
-                                   fn)) != OASIS_OK)
+      (st = oasis::make_stage_args(d, p->local_k, p->local_v, p->local_num_pages, p->local_block_table, ctx_len,
+                                   nullptr, nullptr, nullptr, p->k, nullptr, nullptr, 0, p->k, 1, b.pool_k, b.pool_v,
+                                   nullptr, &la, fn)) != OASIS_OK)
     return st;
   if (d->num_reqs == 0) return ok();
 

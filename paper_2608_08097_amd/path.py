@@ -108,6 +108,8 @@ class DecodePath:
         # created one after another can pass the same pair, which keeps the streams
         # on the hardware queues they were first given
         self.side, self.xfer = streams if streams is not None else (torch.cuda.Stream(), torch.cuda.Stream())
+        # pages a growing step refreshes the local block from (None: the host tier)
+        self.local_source = None
 
     def new_layer(self) -> LayerState:
         return LayerState(self.dims, self.T, self.k, self.block_table.device)
@@ -118,6 +120,8 @@ class DecodePath:
             self._pipe = L.oasis_pipeline_create(self.dims, self.T, self.first_draft, self.num_draft, self.k,
                                                  self.fetch_cap, self.scale, self.host_k, self.host_v,
                                                  self.block_table, self.max_layers, self.side, self.xfer)
+            if self.local_source is not None:
+                L.oasis_pipeline_set_local_source(self._pipe, self.dims, *self.local_source)
         lid = getattr(st, "layer_id", None)
         if lid is None or getattr(st, "pipe", None) != self._pipe:
             if self._n_layers >= self.max_layers:
@@ -129,6 +133,16 @@ class DecodePath:
                                        st.moved, st.out, st.lse, st.ws_attn)
             st.layer_id, st.pipe = lid, self._pipe
         return lid
+
+    def set_local_source(self, k_pages: torch.Tensor | None, v_pages: torch.Tensor | None,
+                         block_table: torch.Tensor | None):
+        """Refresh the local block of growing steps from these pages (bf16 [N][Hkv][B][d], device or
+        pinned, with their own [R][NBmax] block table) instead of the host tier; all None: the host tier.
+        A model writes its newest tokens on the GPU, so keeping the active blocks in device pages keeps
+        the refresh off the PCIe link."""
+        self.local_source = None if k_pages is None else (k_pages, v_pages, block_table)
+        if self._pipe is not None:
+            L.oasis_pipeline_set_local_source(self._pipe, self.dims, k_pages, v_pages, block_table)
 
     def profile_begin(self, max_steps: int):
         """Time every kernel of the next ``max_steps`` native steps on its own stream."""
@@ -175,7 +189,9 @@ class DecodePath:
 
     def refresh_local(self, st: LayerState, ctx_len: torch.Tensor, stream=None):
         """Write the active local block into slot k (stands in for the model's KV write)."""
-        L.oasis_stage_blocks(self.dims, self.host_k, self.host_v, self.block_table, ctx_len, None, None, None,
+        hk, hv, bt = self.local_source if self.local_source is not None else (self.host_k, self.host_v,
+                                                                               self.block_table)
+        L.oasis_stage_blocks(self.dims, hk, hv, bt, ctx_len, None, None, None,
                              self.k, None, None, 0, self.k, True, st.pool_k, st.pool_v, None, stream)
 
     def attend(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, stream=None):

@@ -144,3 +144,14 @@ def gpu_available() -> bool:
 
 def sqrt_d(d: int) -> float:
     return 1.0 / math.sqrt(d)
+
+
+def device_local_pages(w, hk_t, hv_t, steps):
+    """Device copies of the pages that hold a local block during the first ``steps`` steps, and
+    their block table (the active blocks a model would keep on the GPU)."""
+    pages, table = w.local_block_pages(steps)
+    idx = torch.from_numpy(pages)
+    dk = hk_t[idx].cuda() if len(pages) else torch.zeros((1,) + tuple(hk_t.shape[1:]), dtype=hk_t.dtype, device="cuda")
+    dv = hv_t[idx].cuda() if len(pages) else torch.zeros_like(dk)
+    return dk, dv, dev_i32(table)
+

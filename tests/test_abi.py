@@ -118,6 +118,7 @@ def test_pipeline_argument_checks_without_gpu(lib):
     assert L.oasis_pipeline_join(None, None) == 1
     assert L.oasis_pipeline_profile_begin(None, 4) == 1
     assert L.oasis_pipeline_profile_end(None, None, None, None) == 1
+    assert L.oasis_pipeline_set_local_source(None, None, None, 0, None) == 1
     L.oasis_pipeline_destroy(None)
 
 
@@ -126,3 +127,21 @@ def test_workspace_sizes(lib):
     ws = lib.oasis_attn_workspace_bytes(d, 5, 128)
     assert ws > 0 and ws % 4 == 0
     assert lib.oasis_attn_workspace_bytes(lib.dims(1, 32, 8, 64, 16, 1), 5, 4) == 0
+
+
+def test_local_block_pages_cover_every_local_block():
+    """The device copy of the active blocks holds, for every request and step, the block that is
+    local at that step, at the index its table gives."""
+    from workloads import make_workload
+    w = make_workload("c3", num_reqs=4, ctx_args=(16, 1, 40), steps=37, budget=16 * 4)
+    pages, table = w.local_block_pages(37)
+    B = w.cfg.block_size
+    seen = set()
+    for s in range(37):
+        for r, L in enumerate(w.ctx_len(s)):
+            b = (int(L) - 1) // B
+            i = table[r, b]
+            assert i >= 0 and pages[i] == w.block_table[r, b]
+            seen.add((r, b))
+    assert len(seen) == len(pages) == int((table >= 0).sum())
+

@@ -8,8 +8,8 @@ import torch
 import paper_2608_08097_amd as P
 from oracle import oasis_oracle as O
 from paper_2608_08097_amd.path import DecodePath, LayerState
-from tests.gpu_util import (as_np_bits, assert_attn_close, assert_lse_close, dev_bf16, dev_i32, host_bits, note,
-                            pinned_pages, pool_v_to_htd, selection_diff)
+from tests.gpu_util import (as_np_bits, assert_attn_close, assert_lse_close, dev_bf16, dev_i32, device_local_pages,
+                            host_bits, note, pinned_pages, pool_v_to_htd, selection_diff)
 from workloads import make_workload
 
 pytestmark = pytest.mark.gpu
@@ -161,10 +161,12 @@ def test_dense_to_sparse_transition():
     assert_lse_close(st.lse.cpu().numpy(), ref_l)
 
 
-def test_growing_layers_pipelined():
+@pytest.mark.parametrize("local_source", ["host", "device"])
+def test_growing_layers_pipelined(local_source):
     """The reasoning loop of §4.2.2 on the native issuer: several layers, one token appended per
     step, each layer's compressed keys updated when a block completes, capped staging; every
-    layer's output and working set equal its own oracle chain."""
+    layer's output and working set equal its own oracle chain. The local block is refreshed from
+    the host tier, or from device copies of the active blocks (where a model writes new tokens)."""
     n_layers, steps, cap = 3, 40, 3
     w = make_workload("c3", num_reqs=3, ctx_args=(100, 30, 400), steps=steps, budget=16 * 12, ar_queries=True)
     c = w.cfg
@@ -174,6 +176,8 @@ def test_growing_layers_pipelined():
     d = _dims(w)
     bt = dev_i32(w.block_table)
     path = DecodePath(d, c.T, K, hk_t, hv_t, bt, fetch_cap=cap)
+    if local_source == "device":
+        path.set_local_source(*device_local_pages(w, hk_t, hv_t, steps))
     layers = [LayerState(d, c.T, K) for _ in range(n_layers)]
     qs = [w.layer_queries(l, steps) for l in range(n_layers)]
     q_dev = [[dev_bf16(x) for x in qs[l]] for l in range(n_layers)]

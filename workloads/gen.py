@@ -183,6 +183,30 @@ class Workload:
     def ctx_len(self, step: int = 0) -> np.ndarray:
         return (self.ctx0 + self.cfg.grow_per_step * step).astype(np.int32)
 
+    def local_block_pages(self, steps: int) -> tuple[np.ndarray, np.ndarray]:
+        """Pages of the blocks that are a request's local block at some step in [0, steps).
+
+        Returns the host page ids of those blocks (int64, in request and block
+        order) and a [R][NBmax] int32 table that maps each of them to its index
+        in that list (-1 elsewhere): the layout of a small device-resident copy
+        of the active blocks, which a model would write on the GPU.
+        """
+        c = self.cfg
+        B = c.block_size
+        first = self.ctx_len(0).astype(np.int64)
+        last = self.ctx_len(max(0, steps - 1)).astype(np.int64)
+        table = np.full((c.num_reqs, self.NBmax), -1, dtype=np.int32)
+        pages = []
+        for r in range(c.num_reqs):
+            if last[r] <= 0:
+                continue
+            b0 = max(0, int(first[r] - 1) // B)
+            b1 = int(last[r] - 1) // B
+            for b in range(b0, b1 + 1):
+                table[r, b] = len(pages)
+                pages.append(int(self.block_table[r, b]))
+        return np.array(pages, dtype=np.int64), table
+
     def n_cand0(self, r: int) -> int:
         B = self.cfg.block_size
         return int((int(self.ctx0[r]) + B - 1) // B - 1)

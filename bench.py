@@ -423,13 +423,14 @@ def run_reasoning(args, P, torch, DecodePath):
 
     32 layers, 64 requests with a 1K prompt plus 4K-16K generated tokens, block
     16, 4 draft tokens, budget 2,048; 64 consecutive decode steps, one token
-    appended per request per step. Per step and layer: the compressed keys of a
-    block that just completed are added (oasis_update_summaries), the local
-    block is refreshed, and the pipelined step runs (attention on the
-    foreground, prediction and capped staging behind it). The host K/V tier is
-    shared by the layers; each layer has its own summaries, working set and
-    query stream. The active (local) blocks are device-resident, standing in for
-    the model's own KV writes, so only the delta transfer crosses PCIe. Queries follow the AR(1) recipe, drawn on the GPU from a
+    appended per request per step. Per step and layer, one pipelined step: the
+    local block is refreshed and attended on the foreground; the compressed keys
+    of a block that just completed are added, then scoring and top-K run on the
+    prediction stream; capped staging follows on the transfer stream. The host
+    K/V tier is shared by the layers; each layer has its own summaries, working
+    set and query stream. The active (local) blocks are device-resident,
+    standing in for the model's own KV writes, so only the delta transfer
+    crosses PCIe. Queries follow the AR(1) recipe, drawn on the GPU from a
     seeded generator (2.7 G values would take a minute to draw on the host).
     Reports tokens/s, layer-steps/s, and T_pipe against Delta_prefetch =
     T_step / N_layer.
@@ -493,9 +494,9 @@ def run_reasoning(args, P, torch, DecodePath):
     def decode():
         for s_ in range(S):
             for l, st in enumerate(layers):
-                if s_:
-                    P.oasis_update_summaries(d, dev_k, dev_bt, ctx_d[s_ - 1], ctx_d[s_], 1, st.kmax, st.kmin)
-                path.step_pipelined(st, qs[l][s_], ctx_d[s_], s_, growing=True, moved=moved_log[s_, l])
+                # the step adds the compressed keys of a block that just completed (prediction stream)
+                path.step_pipelined(st, qs[l][s_], ctx_d[s_], s_, growing=True, moved=moved_log[s_, l],
+                                    prev_ctx_len=ctx_d[s_ - 1] if s_ else None)
         path.join()
         torch.cuda.synchronize()
 

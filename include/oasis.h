@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define OASIS_ABI_VERSION 3
+#define OASIS_ABI_VERSION 4
 
 /* Only the entry points below are exported from liboasis.so. */
 #if defined(__GNUC__) || defined(__clang__)
@@ -356,11 +356,17 @@ OASIS_API oasis_status oasis_pipeline_set_local_source(oasis_pipeline* pipeline,
                                              const int32_t* block_table);
 
 /* Issue one decode step of `layer` (see above). q: bf16 device [R][T][Hq][d];
- * ctx_len: device [R]; step: the stamp of this step's selection; moved: where
- * the transfer writes its per-(r, h) entry counts (NULL: the layer's buffer). */
+ * ctx_len: device [R]; prev_ctx_len (nullable, device [R]): the lengths at the
+ * layer's previous step; when set, the compressed keys of the blocks completed
+ * since then (at most max_new_blocks >= 1 per request) are added on the
+ * prediction stream before the scoring (as oasis_update_summaries, reading the
+ * local-block source, where the newest tokens are), so that this small kernel
+ * does not wait behind the scan on the foreground; step: the stamp of this
+ * step's selection; moved: where the transfer writes its per-(r, h) entry
+ * counts (NULL: the layer's buffer). */
 OASIS_API oasis_status oasis_pipeline_step(oasis_pipeline* pipeline, int32_t layer, const uint16_t* q,
-                                 const int32_t* ctx_len, int32_t step, int32_t growing, int32_t* moved,
-                                 void* stream);
+                                 const int32_t* ctx_len, const int32_t* prev_ctx_len, int32_t max_new_blocks,
+                                 int32_t step, int32_t growing, int32_t* moved, void* stream);
 
 /* Make `stream` wait for all work issued so far on the two background streams. */
 OASIS_API oasis_status oasis_pipeline_join(oasis_pipeline* pipeline, void* stream);

@@ -58,7 +58,7 @@ def dims(num_reqs, num_q_heads, num_kv_heads, head_dim, block_size, max_blocks) 
 
 
 _lib = None
-ABI_VERSION = 3  # OASIS_ABI_VERSION of include/oasis.h
+ABI_VERSION = 4  # OASIS_ABI_VERSION of include/oasis.h
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -110,7 +110,7 @@ def lib() -> ctypes.CDLL:
         L.oasis_pipeline_set_local_source.restype = _I32
         L.oasis_pipeline_set_local_source.argtypes = [_P, _P, _P, _I64, _P]
         L.oasis_pipeline_step.restype = _I32
-        L.oasis_pipeline_step.argtypes = [_P, _I32, _P, _P, _I32, _I32, _P, _P]
+        L.oasis_pipeline_step.argtypes = [_P, _I32, _P, _P, _P, _I32, _I32, _I32, _P, _P]
         L.oasis_pipeline_join.restype = _I32
         L.oasis_pipeline_join.argtypes = [_P, _P]
         L.oasis_pipeline_destroy.restype = None
@@ -379,15 +379,18 @@ def oasis_pipeline_set_layer(handle: int, layer: int, d: OasisDims, num_q_tokens
 
 
 def oasis_pipeline_step(handle: int, layer: int, q, ctx_len, step: int, growing: bool, moved=None,
-                        stream=None) -> None:
-    """One layer's pipelined step (q, ctx_len, moved: device tensors of the pipeline's shapes)."""
+                        stream=None, prev_ctx_len=None, max_new_blocks: int = 1) -> None:
+    """One layer's pipelined step (q, ctx_len, prev_ctx_len, moved: device tensors of the pipeline's
+    shapes); with prev_ctx_len the compressed keys of newly completed blocks are added first."""
     nq, nr, nm = _PIPE_SIZES[handle]
     _need(q, nq, "q")
     _need(ctx_len, nr, "ctx_len")
+    _need(prev_ctx_len, nr, "prev_ctx_len")
     _need(moved, nm, "moved")
     _check("oasis_pipeline_step", lib().oasis_pipeline_step(
-        handle, int(layer), _dev(q, "q", _BF16), _dev(ctx_len, "ctx_len", _I32T), int(step), 1 if growing else 0,
-        _dev(moved, "moved", _I32T, nullable=True), _stream(stream)))
+        handle, int(layer), _dev(q, "q", _BF16), _dev(ctx_len, "ctx_len", _I32T),
+        _dev(prev_ctx_len, "prev_ctx_len", _I32T, nullable=True), int(max_new_blocks), int(step),
+        1 if growing else 0, _dev(moved, "moved", _I32T, nullable=True), _stream(stream)))
 
 
 def oasis_pipeline_join(handle: int, stream=None) -> None:

@@ -250,12 +250,15 @@ oasis_status oasis_pipeline_set_layer(oasis_pipeline* p, int32_t layer, const oa
 }
 
 oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_t* q, const int32_t* ctx_len,
-                                 int32_t step, int32_t growing, int32_t* moved, void* stream) {
+                                 const int32_t* prev_ctx_len, int32_t max_new_blocks, int32_t step, int32_t growing,
+                                 int32_t* moved, void* stream) {
   static const char* fn = "oasis_pipeline_step";
   if (!p) return fail(OASIS_ERR_INVALID_ARG, "%s: pipeline is NULL", fn);
   if (layer < 0 || layer >= p->max_layers || !p->is_set[layer])
     return fail(OASIS_ERR_INVALID_ARG, "%s: layer %d has no buffers (oasis_pipeline_set_layer)", fn, layer);
   if (growing != 0 && growing != 1) return fail(OASIS_ERR_INVALID_ARG, "%s: growing must be 0 or 1", fn);
+  if (prev_ctx_len && max_new_blocks < 1)
+    return fail(OASIS_ERR_INVALID_ARG, "%s: max_new_blocks = %d < 1", fn, max_new_blocks);
   const oasis_layer_buffers& b = p->layers[layer];
   const oasis_dims* d = &p->dims;
   oasis::AttnArgs aa{};
@@ -280,6 +283,11 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
                                    nullptr, &la, fn)) != OASIS_OK)
     return st;
   if (d->num_reqs == 0) return ok();
+  // compressed keys of the blocks completed since prev_ctx_len, read from the
+  // local-block source (where the newest tokens are), before the scoring
+  const oasis::SummaryArgs ua{p->local_k, p->local_num_pages, p->local_block_table, ctx_len, b.kmax, b.kmin,
+                              d->num_reqs, d->num_kv_heads, d->block_size, d->max_blocks, prev_ctx_len,
+                              max_new_blocks};
 
   hipStream_t fg = static_cast<hipStream_t>(stream);
   bool near_wrap = p->staged[layer] >= kWrapGuard;
@@ -296,6 +304,7 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   if (growing) HIP_TRY(oasis::launch_stage(la, fg), fn);
   HIP_TRY(oasis::launch_attn(aa, fg, prof_timing(p, 0)), fn);
   HIP_TRY(signal(p, fg, kAttn, ++cnt[kAttn]), fn);
+  if (prev_ctx_len) HIP_TRY(oasis::launch_summaries(ua, p->pred), fn);
   HIP_TRY(oasis::launch_score(sa, p->pred, prof_timing(p, 1)), fn);
   HIP_TRY(oasis::launch_topk(ta, p->pred, prof_timing(p, 2)), fn);
   HIP_TRY(signal(p, p->pred, kPred, ++cnt[kPred]), fn);

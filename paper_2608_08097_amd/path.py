@@ -206,7 +206,8 @@ class DecodePath:
         self.attend(st, q, ctx_len)
 
     def step_pipelined(self, st: LayerState, q: torch.Tensor, ctx_len: torch.Tensor, step: int,
-                       growing: bool = False, timer: KernelTimer | None = None, moved: torch.Tensor | None = None):
+                       growing: bool = False, timer: KernelTimer | None = None, moved: torch.Tensor | None = None,
+                       prev_ctx_len: torch.Tensor | None = None, max_new_blocks: int = 1):
         """One steady-state step of one layer (paper §4.2.2 pipeline).
 
         Foreground (current stream): wait for this layer's previous transfer,
@@ -223,14 +224,17 @@ class DecodePath:
         initial fill stages it) and nothing moves it.
         ``timer`` records HIP events around each call on its own stream;
         ``moved`` (int32 [R][Hkv]) receives the entries this step copies.
+        With ``prev_ctx_len`` (the lengths at this layer's previous step) the
+        compressed keys of the blocks completed since then are added on the
+        prediction stream before the scoring, read from the local-block source.
         Without a timer the step goes through the library's native issuer (one
         C call); with one it is issued call by call from here. Switching between
         the two for one layer needs a device synchronization in between.
         """
         if timer is None and self.native:
             lid = self._native_layer(st)
-            L.oasis_pipeline_step(self._pipe, lid, q, ctx_len, step, growing, moved,
-                                  torch.cuda.current_stream())
+            L.oasis_pipeline_step(self._pipe, lid, q, ctx_len, step, growing, moved, torch.cuda.current_stream(),
+                                  prev_ctx_len, max_new_blocks)
             return
         tm = timer if timer is not None else _NO_TIMER
         fg = torch.cuda.current_stream()
@@ -248,6 +252,11 @@ class DecodePath:
         tm.end("attn", fg, e)
         ev_attn = torch.cuda.Event()
         ev_attn.record(fg)
+        if prev_ctx_len is not None:
+            hk, _, bt = self.local_source if self.local_source is not None else (self.host_k, self.host_v,
+                                                                                 self.block_table)
+            L.oasis_update_summaries(self.dims, hk, bt, prev_ctx_len, ctx_len, max_new_blocks, st.kmax, st.kmin,
+                                     pred)
         e = tm.begin("score", pred)
         L.oasis_score_blocks(self.dims, q, self.T, self.first_draft, self.num_draft, st.kmax, st.kmin, ctx_len,
                              st.scores, pred)

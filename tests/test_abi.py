@@ -48,7 +48,7 @@ def test_exports_match_header(lib):
 
 
 def test_abi_version(lib):
-    assert lib.oasis_abi_version() == 3
+    assert lib.oasis_abi_version() == 4
 
 
 def test_argument_checks_without_gpu(lib):
@@ -114,7 +114,7 @@ def test_pipeline_argument_checks_without_gpu(lib):
     assert L.oasis_pipeline_create(ctypes.byref(d), 5, 1, 4, 128, 6, 1.0, None, None, 10, None, 8, 1, None,
                                    ctypes.byref(h)) == 1
     assert L.oasis_pipeline_set_layer(None, 0, None) == 1
-    assert L.oasis_pipeline_step(None, 0, None, None, 0, 0, None, None) == 1
+    assert L.oasis_pipeline_step(None, 0, None, None, None, 0, 0, 0, None, None) == 1
     assert L.oasis_pipeline_join(None, None) == 1
     assert L.oasis_pipeline_profile_begin(None, 4) == 1
     assert L.oasis_pipeline_profile_end(None, None, None, None) == 1

@@ -166,7 +166,8 @@ def test_growing_layers_pipelined(local_source):
     """The reasoning loop of §4.2.2 on the native issuer: several layers, one token appended per
     step, each layer's compressed keys updated when a block completes, capped staging; every
     layer's output and working set equal its own oracle chain. The local block is refreshed from
-    the host tier, or from device copies of the active blocks (where a model writes new tokens)."""
+    the host tier with the compressed keys updated by the caller, or from device copies of the
+    active blocks (where a model writes new tokens) with the update issued by the step itself."""
     n_layers, steps, cap = 3, 40, 3
     w = make_workload("c3", num_reqs=3, ctx_args=(100, 30, 400), steps=steps, budget=16 * 12, ar_queries=True)
     c = w.cfg
@@ -194,9 +195,13 @@ def test_growing_layers_pipelined(local_source):
     note("growing layers: issuing all steps")
     for s in range(steps):
         for l, st in enumerate(layers):
-            if s > 0:
-                P.oasis_update_summaries(d, hk_t, bt, ctx_dev[s - 1], ctx_dev[s], 1, st.kmax, st.kmin)
-            path.step_pipelined(st, q_dev[l][s], ctx_dev[s], s, growing=True)
+            if local_source == "host":   # compressed keys updated by the caller, on the foreground
+                if s > 0:
+                    P.oasis_update_summaries(d, hk_t, bt, ctx_dev[s - 1], ctx_dev[s], 1, st.kmax, st.kmin)
+                path.step_pipelined(st, q_dev[l][s], ctx_dev[s], s, growing=True)
+            else:                        # by the step, on the prediction stream, from the device pages
+                path.step_pipelined(st, q_dev[l][s], ctx_dev[s], s, growing=True,
+                                    prev_ctx_len=ctx_dev[s - 1] if s > 0 else None)
     path.join()
     torch.cuda.synchronize()
     none_sel = np.full((c.num_reqs, H, K), -1, np.int32)

@@ -548,6 +548,11 @@ def test_pipeline_abi_errors_on_device():
         with pytest.raises(P.OasisError) as e:  # workspace too small, caught by the per-step checks
             P.oasis_pipeline_step(h, 0, q, ctx, 0, False)
         assert e.value.status == 4
+        with pytest.raises(P.OasisError) as e:  # a summary update with no room for a new block
+            P.oasis_pipeline_step(h, 0, q, ctx, 0, True, prev_ctx_len=ctx, max_new_blocks=0)
+        assert e.value.status == 1 and "max_new_blocks" in str(e.value)
+        # a local-block source needs all three of k_pages, v_pages and block_table
+        assert P._lib.lib().oasis_pipeline_set_local_source(h, hk_t.data_ptr(), None, 1, None) == 1
         with pytest.raises(P.OasisError) as e:
             P.oasis_pipeline_set_layer(h, 4, d, c.T, c.K, st.kmax, st.kmin, st.scores, st.sel, st.sel_count,
                                        st.slot_map, st.slot_stamp, st.pool_k, st.pool_v, st.moved, st.out,

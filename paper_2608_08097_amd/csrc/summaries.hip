@@ -4,15 +4,18 @@
 // previous context length (§5.1 compressed-key updates).
 //
 // One thread owns 8 consecutive dimensions of one (request, block, KV head) and
-// walks the B tokens of the page with 16-byte loads; neighbouring threads cover
-// neighbouring dimensions, so a wave reads whole 256-byte key rows. The result
-// is exact: min/max of bf16 values is a bf16 value.
+// reads the B tokens of the page with 16-byte loads, all issued before the
+// first is used (B is a template parameter, so the token loop unrolls);
+// neighbouring threads cover neighbouring dimensions, so a wave reads whole
+// 256-byte key rows. The result is exact: min/max of bf16 values is a bf16
+// value.
 #include "oasis_internal.h"
 
 namespace oasis {
 
 namespace {
 
+template <int BS>
 __global__ __launch_bounds__(256) void summaries_kernel(SummaryArgs a) {
   const int r = blockIdx.y;
   const long long item = (long long)blockIdx.x * blockDim.x + threadIdx.x;
@@ -20,23 +23,27 @@ __global__ __launch_bounds__(256) void summaries_kernel(SummaryArgs a) {
   const int rem = (int)(item % per_block);
   const int h = rem / (kHeadDim / 8);
   const int d0 = (rem % (kHeadDim / 8)) * 8;
-  const Ctx c = ctx_blocks(a.ctx_len[r], a.B, a.NBmax);
+  const Ctx c = ctx_blocks(a.ctx_len[r], BS, a.NBmax);
   // update form: the grid covers max_new blocks per request, from the first one completed since prev
-  const int lo = a.prev_ctx_len ? ctx_blocks(a.prev_ctx_len[r], a.B, a.NBmax).n_cand : 0;
+  const int lo = a.prev_ctx_len ? ctx_blocks(a.prev_ctx_len[r], BS, a.NBmax).n_cand : 0;
   const int b = lo + (int)(item / per_block);
   if (b >= c.n_cand || (a.prev_ctx_len && b >= lo + a.max_new)) return;
   const int page = a.block_table[(long long)r * a.NBmax + b];
   if (page < 0 || page >= a.num_pages) return;
 
-  const uint16_t* src = a.k_pages + (((long long)page * a.Hkv + h) * a.B) * kHeadDim + d0;
+  const uint16_t* src = a.k_pages + (((long long)page * a.Hkv + h) * BS) * kHeadDim + d0;
   float mx[8], mn[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     mx[j] = -INFINITY;
     mn[j] = INFINITY;
   }
-  for (int p = 0; p < a.B; ++p) {
-    const u32x4 v = ldg16(src + (long long)p * kHeadDim);
+  u32x4 rows[BS];
+#pragma unroll
+  for (int p = 0; p < BS; ++p) rows[p] = ldg16(src + (long long)p * kHeadDim);
+#pragma unroll
+  for (int p = 0; p < BS; ++p) {
+    const u32x4 v = rows[p];
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const float lo = bf16_bits_to_f32(v[w] & 0xFFFFu);
@@ -65,7 +72,12 @@ hipError_t launch_summaries(const SummaryArgs& a, hipStream_t s) {
   const long long blocks = a.prev_ctx_len ? (a.max_new < a.NBmax ? a.max_new : a.NBmax) : a.NBmax;
   const long long items = blocks * a.Hkv * (kHeadDim / 8);
   const dim3 grid((unsigned)((items + 255) / 256), (unsigned)a.R);
-  hipLaunchKernelGGL(summaries_kernel, grid, dim3(256), 0, s, a);
+  if (a.B == 16)
+    hipLaunchKernelGGL(summaries_kernel<16>, grid, dim3(256), 0, s, a);
+  else if (a.B == 32)
+    hipLaunchKernelGGL(summaries_kernel<32>, grid, dim3(256), 0, s, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -50,6 +50,7 @@ constexpr int kKeyPad = 4;
 constexpr int kCopyWorkgroupsMin = 32;
 constexpr int kCopyWorkgroupsMax = 64;
 constexpr int kCopyInflightMin = 64;  // block-head entries (K and V) in flight over the whole grid, at least
+constexpr int kLocalWorkgroups = 256;  // grid of a local-block-only call
 
 // Monotone map of a float onto uint32 (larger float, larger key; -0 and +0 equal).
 __device__ inline unsigned order_key(float f) {
@@ -370,6 +371,8 @@ hipError_t launch_bs(const StageArgs& a, hipStream_t s, const LaunchTiming& t) {
   if (nrh <= 0) return hipSuccess;
   int grid = nrh / 2;
   grid = grid < kCopyWorkgroupsMin ? kCopyWorkgroupsMin : (grid > kCopyWorkgroupsMax ? kCopyWorkgroupsMax : grid);
+  // the local block alone (no plan, one entry per pair, on the caller's critical path): spread wide
+  if (a.local_only) grid = nrh < kLocalWorkgroups ? nrh : kLocalWorkgroups;
   if (grid > nrh) grid = nrh;
   const int pf = grid * 2 >= kCopyInflightMin ? 2 : kCopyInflightMin / grid;  // entries per workgroup batch
   if (pf >= 8)

@@ -81,8 +81,13 @@ __device__ void select_row(const float* s, int n, int k, int32_t* out, int32_t* 
   constexpr int kRegs = KPT > 0 ? KPT : 1;
   uint32_t keys[kRegs];
   if (KPT > 0) {
+    // every load is issued (index clamped into the row, n > k >= 1 here) before
+    // any is used; keys past this thread's range are masked afterwards
 #pragma unroll
-    for (int j = 0; j < kRegs; ++j) keys[j] = j < cnt_local ? select_key(s[lo + j]) : 0u;
+    for (int j = 0; j < kRegs; ++j) {
+      const uint32_t key = select_key(s[min(lo + j, n - 1)]);
+      keys[j] = j < cnt_local ? key : 0u;
+    }
   }
   auto key_at = [&](int j) -> uint32_t { return KPT > 0 ? keys[j] : select_key(s[lo + j]); };
   const int jmax = KPT > 0 ? kRegs : cnt_local;

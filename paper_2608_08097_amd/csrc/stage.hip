@@ -17,10 +17,11 @@
 //          thread (misses by score under a cap, stale slots by (stamp, slot));
 //          slot_map / slot_stamp are updated in place and the (slot, page)
 //          pairs stay in LDS;
-//   copy   the entries are streamed in batches of PF: the PCIe loads of a
-//          whole batch (PF x 2 x B x d x 2 bytes) are issued before any is
-//          stored, K goes to the pool token-major, V is transposed through LDS
-//          into the d x B layout the attention kernel reads.
+//   copy   the entries are streamed in batches of PF with two batches in
+//          flight: the PCIe loads of the next batch are issued before the
+//          current one is stored; K goes to the pool token-major, V is
+//          transposed through LDS into the d x B layout the attention kernel
+//          reads.
 // Host reads take microseconds to return, so the plans run in parallel and
 // each workgroup keeps a batch of entries in flight. Host reads beyond what
 // saturates the link only queue inside the GPU, where they slow the HBM
@@ -28,8 +29,12 @@
 // 8 entries per workgroup in flight on 64 workgroups stretch a concurrent
 // block scan from 57 to 98 us, 2 entries to 88 us). The grid is therefore one
 // workgroup per two pairs, kept between kCopyWorkgroupsMin and
-// kCopyWorkgroupsMax, with 2 entries in flight per workgroup (more on small
-// grids, so that the link still fills). Measured step rates (steps/s) for
+// kCopyWorkgroupsMax, with 2 entries in flight per workgroup (1 per batch;
+// more on small grids, so that the link still fills). Keeping the second
+// batch in flight while the first is stored raised the reasoning loop of
+// 32 layers x 64 requests from 6,300 to 6,710 tokens/s (the transfer there
+// paces the step) and changed 8 x 131,072 tokens by -1 %. Step rates measured
+// before that change (steps/s) for
 // 32 / 48 / 64 workgroups: 8 x 131,072 tokens (64 pairs) 10,490 / 9,790 /
 // 9,290; 32 requests of 16K-32K tokens (256 pairs) 7,920 / 8,540 / 8,400;
 // 16 x 65,536 tokens with B = 32 (128 pairs) 3,510 / 3,510 / 3,700. Fewer
@@ -281,13 +286,89 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
   return n_adm;
 }
 
+// One batch of PF block-head entries held in registers (K and V, 16-byte
+// chunks of each entry spread over the workgroup).
+template <int BS, int PF>
+struct CopyBatch {
+  static constexpr int kChunks = BS * kHeadDim / 8 / kPlanThreads;
+  u32x4 k[PF][kChunks], v[PF][kChunks];
+  int slot[PF], page[PF];
+};
+
+template <int BS, int PF>
+__device__ __forceinline__ void fetch_batch(const StageArgs& a, CopyBatch<BS, PF>& b, int e0, int n, int r, int h,
+                                            const int* s_slot, const int* s_page) {
+  constexpr int kElems = BS * kHeadDim;
+  const int tid = threadIdx.x;
+  // placeholder source: slot 0 of this (r, h) in the pool
+  const long long hold = (((long long)r * (a.k + 1)) * a.Hkv + h) * kElems;
+#pragma unroll
+  for (int p = 0; p < PF; ++p) {
+    const int e = e0 + p;
+    b.slot[p] = e < n ? s_slot[e] : -1;
+    b.page[p] = e < n ? s_page[e] : -1;
+    const bool live = b.page[p] >= 0 && b.slot[p] >= 0 && b.slot[p] <= a.k;
+    if (!live) b.page[p] = -1;
+    const long long src = ((long long)(live ? b.page[p] : 0) * a.Hkv + h) * kElems;
+    const uint16_t* ks = live ? a.host_k + src : a.pool_k + hold;
+    const uint16_t* vs = live ? a.host_v + src : a.pool_k + hold;
+#pragma unroll
+    for (int q = 0; q < CopyBatch<BS, PF>::kChunks; ++q) {
+      const int c = (q * kPlanThreads + tid) * 8;
+      b.k[p][q] = ldg16(ks + c);
+      b.v[p][q] = ldg16(vs + c);
+    }
+  }
+}
+
+// Store a fetched batch: K token-major into the pool, V transposed through LDS
+// into the d x B layout the attention kernel reads.
+template <int BS, int PF>
+__device__ __forceinline__ void put_batch(const StageArgs& a, const CopyBatch<BS, PF>& b, int r, int h,
+                                          uint16_t (*tile)[BS * kHeadDim]) {
+  constexpr int kElems = BS * kHeadDim;
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int p = 0; p < PF; ++p) {
+    if (b.page[p] < 0) continue;
+    const long long dst = (((long long)r * (a.k + 1) + b.slot[p]) * a.Hkv + h) * kElems;
+#pragma unroll
+    for (int q = 0; q < CopyBatch<BS, PF>::kChunks; ++q) {
+      const int c = (q * kPlanThreads + tid) * 8;
+      *reinterpret_cast<u32x4*>(a.pool_k + dst + c) = b.k[p][q];
+      *reinterpret_cast<u32x4*>(&tile[p][c]) = b.v[p][q];
+    }
+  }
+  __syncthreads();
+  // V: [BS][d] -> [d][BS]; thread -> (d, 8-token group)
+  constexpr int kGroups = BS / 8;
+#pragma unroll
+  for (int p = 0; p < PF; ++p) {
+    if (b.page[p] < 0) continue;
+    const long long dst = (((long long)r * (a.k + 1) + b.slot[p]) * a.Hkv + h) * kElems;
+#pragma unroll
+    for (int w = tid; w < kHeadDim * kGroups; w += kPlanThreads) {
+      const int d = w / kGroups;
+      const int t0 = (w % kGroups) * 8;
+      u32x4 o;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t lo = tile[p][(t0 + 2 * j) * kHeadDim + d];
+        const uint32_t hi = tile[p][(t0 + 2 * j + 1) * kHeadDim + d];
+        o[j] = lo | (hi << 16);
+      }
+      *reinterpret_cast<u32x4*>(a.pool_v + dst + (long long)d * BS + t0) = o;
+    }
+  }
+  __syncthreads();
+}
+
 template <int BS, int PF>
 __global__ __launch_bounds__(kPlanThreads) void stage_kernel(StageArgs a) {
   const int tid = threadIdx.x;
   __shared__ int s_slot[kMaxK + 1], s_page[kMaxK + 1];
   __shared__ int s_wave[8];
   constexpr int kElems = BS * kHeadDim;          // one K (or V) block-head entry
-  constexpr int kChunks = kElems / 8 / kPlanThreads;  // 16-byte chunks per thread
   __shared__ uint16_t tile[PF][kElems];
 
   for (int rh = blockIdx.x; rh < a.R * a.Hkv; rh += gridDim.x) {
@@ -307,57 +388,19 @@ __global__ __launch_bounds__(kPlanThreads) void stage_kernel(StageArgs a) {
   }
   __syncthreads();
 
-  for (int e0 = 0; e0 < n; e0 += PF) {
-    u32x4 kr[PF][kChunks], vr[PF][kChunks];
-    int slot[PF], page[PF];
-#pragma unroll
-    for (int p = 0; p < PF; ++p) {
-      const int e = e0 + p;
-      slot[p] = e < n ? s_slot[e] : -1;
-      page[p] = e < n ? s_page[e] : -1;
-      const bool live = page[p] >= 0 && slot[p] >= 0 && slot[p] <= a.k;
-      if (!live) page[p] = -1;
-      const long long src = ((long long)(live ? page[p] : 0) * a.Hkv + h) * kElems;
-#pragma unroll
-      for (int q = 0; q < kChunks; ++q) {
-        const int c = (q * kPlanThreads + tid) * 8;
-        kr[p][q] = live ? ldg16(a.host_k + src + c) : u32x4{0, 0, 0, 0};
-        vr[p][q] = live ? ldg16(a.host_v + src + c) : u32x4{0, 0, 0, 0};
-      }
-    }
-#pragma unroll
-    for (int p = 0; p < PF; ++p) {
-      if (page[p] < 0) continue;
-      const long long dst = (((long long)r * (a.k + 1) + slot[p]) * a.Hkv + h) * kElems;
-#pragma unroll
-      for (int q = 0; q < kChunks; ++q) {
-        const int c = (q * kPlanThreads + tid) * 8;
-        *reinterpret_cast<u32x4*>(a.pool_k + dst + c) = kr[p][q];
-        *reinterpret_cast<u32x4*>(&tile[p][c]) = vr[p][q];
-      }
-    }
-    __syncthreads();
-    // V: [BS][d] -> [d][BS]; thread -> (d, 8-token group)
-    constexpr int kGroups = BS / 8;
-#pragma unroll
-    for (int p = 0; p < PF; ++p) {
-      if (page[p] < 0) continue;
-      const long long dst = (((long long)r * (a.k + 1) + slot[p]) * a.Hkv + h) * kElems;
-#pragma unroll
-      for (int w = tid; w < kHeadDim * kGroups; w += kPlanThreads) {
-        const int d = w / kGroups;
-        const int t0 = (w % kGroups) * 8;
-        u32x4 o;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t lo = tile[p][(t0 + 2 * j) * kHeadDim + d];
-          const uint32_t hi = tile[p][(t0 + 2 * j + 1) * kHeadDim + d];
-          o[j] = lo | (hi << 16);
-        }
-        *reinterpret_cast<u32x4*>(a.pool_v + dst + (long long)d * BS + t0) = o;
-      }
-    }
-    __syncthreads();
+  // Batches of PF entries, two in flight: the host reads of the next batch are
+  // issued before the current one is stored, so the link does not idle while
+  // a batch is written and V is transposed. Every load is issued; an entry
+  // past the end (or without a page) reads slot 0 of this (r, h) in the pool
+  // instead (device memory, discarded), so the wait counts stay exact.
+  CopyBatch<BS, PF> x, y;
+  fetch_batch<BS, PF>(a, x, 0, n, r, h, s_slot, s_page);
+  for (int e0 = 0; e0 < n; e0 += 2 * PF) {
+    fetch_batch<BS, PF>(a, y, e0 + PF, n, r, h, s_slot, s_page);
+    put_batch<BS, PF>(a, x, r, h, tile);
+    if (e0 + PF >= n) break;
+    fetch_batch<BS, PF>(a, x, e0 + 2 * PF, n, r, h, s_slot, s_page);
+    put_batch<BS, PF>(a, y, r, h, tile);
   }
   __syncthreads();  // LDS plan arrays are reused by the next pair
   }
@@ -374,7 +417,8 @@ hipError_t launch_bs(const StageArgs& a, hipStream_t s, const LaunchTiming& t) {
   // the local block alone (no plan, one entry per pair, on the caller's critical path): spread wide
   if (a.local_only) grid = nrh < kLocalWorkgroups ? nrh : kLocalWorkgroups;
   if (grid > nrh) grid = nrh;
-  const int pf = grid * 2 >= kCopyInflightMin ? 2 : kCopyInflightMin / grid;  // entries per workgroup batch
+  // entries per batch; two batches are in flight per workgroup
+  const int pf = grid * 2 >= kCopyInflightMin ? 1 : kCopyInflightMin / (2 * grid);
   if (pf >= 8)
     launch_kernel(stage_kernel<BS, 8>, dim3(grid), dim3(kPlanThreads), s, t, a);
   else if (pf >= 4)

@@ -22,13 +22,25 @@ __global__ __launch_bounds__(kThreads) void union_kernel(UnionArgs a) {
   const int words = (a.NBmax + 31) / 32;
   for (int w = tid; w < words; w += kThreads) bm[w] = 0u;
   __syncthreads();
-  for (int h = 0; h < a.Hkv; ++h) {
-    const long long rh = (long long)r * a.Hkv + h;
-    int m = a.sel_count[rh];
-    m = m < 0 ? 0 : (m > a.k ? a.k : m);
-    for (int i = tid; i < m; i += kThreads) {
-      const int b = a.sel[rh * a.k + i];
-      if (b >= 0 && b < a.NBmax) atomicOr(&bm[b >> 5], 1u << (b & 31));
+  // (head, entry) pairs of the request, four per thread at a time; the count
+  // and the id of an entry are loaded together, so the loads of a group are
+  // all in flight before any is used
+  const int pairs = a.Hkv * a.k;
+  const long long row0 = (long long)r * a.Hkv;
+  for (int base = 0; base < pairs; base += 4 * kThreads) {
+    int b[4], m[4], i[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int idx = base + u * kThreads + tid;
+      const int h = idx < pairs ? idx / a.k : 0;
+      i[u] = idx < pairs ? idx - h * a.k : a.k;
+      m[u] = a.sel_count[row0 + h];
+      b[u] = a.sel[(row0 + h) * a.k + (i[u] < a.k ? i[u] : 0)];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int mm = m[u] < 0 ? 0 : (m[u] > a.k ? a.k : m[u]);
+      if (i[u] < mm && b[u] >= 0 && b[u] < a.NBmax) atomicOr(&bm[b[u] >> 5], 1u << (b[u] & 31));
     }
   }
   __syncthreads();

@@ -119,7 +119,8 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
     pg[j] = -1;
     ky[j] = 0u;
     if (i < k) {
-      const int b = i < m ? a.sel[base + i] : INT_MAX;
+      const int sv = a.sel[base + i];  // in the row (k entries); loaded without waiting for the count
+      const int b = i < m ? sv : INT_MAX;
       s_sel[i] = b;
       s_hit[i] = 0;
       s_map[i] = a.slot_map[base + i];

@@ -47,6 +47,9 @@ CASES = {
     "g4_d6": lambda: make_workload("c2", num_reqs=2, num_draft=6, ctx_args=(900, 2600), budget=384),
     # G = 8, D = 6, B = 32: 48 scoring rows (three row tiles), 56 attention rows (four tiles)
     "g8_d6_b32": lambda: make_workload("c5", num_reqs=2, num_draft=6, ctx_args=(2000,), budget=512),
+    # 2 requests x 2 KV heads: a staging grid of 4 workgroups with batches of 8 entries
+    "h2": lambda: make_workload("c2", num_reqs=2, num_q_heads=8, num_kv_heads=2, ctx_args=(600, 2500),
+                                budget=16 * 20),
 }
 
 

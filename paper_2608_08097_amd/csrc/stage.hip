@@ -11,35 +11,42 @@
 // writes them into the resident GPU pages.
 //
 // A grid of 256-thread workgroups walks the (request, KV head) pairs
-// (workgroup w takes pairs w, w + grid, ...); for each pair it does:
-//   plan   the slot map, stamps and selection sit in LDS; misses and stale
-//          slots are compacted by workgroup scans and ranked one item per
-//          thread (misses by score under a cap, stale slots by (stamp, slot));
-//          slot_map / slot_stamp are updated in place and the (slot, page)
-//          pairs stay in LDS;
-//   copy   the entries are streamed in batches of PF with two batches in
-//          flight: the PCIe loads of the next batch are issued before the
-//          current one is stored; K goes to the pool token-major, V is
-//          transposed through LDS into the d x B layout the attention kernel
-//          reads.
+// (workgroup w takes pairs w, w + grid, ...), as many pairs per pass as the
+// LDS plan arrays hold (kMaxK / k, at most kMaxPairs); each pass does:
+//   plan   the slot maps, stamps and selections of the pass's pairs sit in
+//          LDS side by side; misses and stale slots are compacted by
+//          workgroup scans and ranked one item per thread within their pair
+//          (misses by score under a cap, stale slots by (stamp, slot));
+//          slot_map / slot_stamp are updated in place and the (slot, page,
+//          pair) entries stay in LDS;
+//   copy   the entries of all the pass's pairs are streamed in batches of PF
+//          with two batches in flight: the PCIe loads of the next batch are
+//          issued before the current one is stored; K goes to the pool
+//          token-major, V is transposed through LDS into the d x B layout the
+//          attention kernel reads.
 // Host reads take microseconds to return, so the plans run in parallel and
-// each workgroup keeps a batch of entries in flight. Host reads beyond what
-// saturates the link only queue inside the GPU, where they slow the HBM
-// traffic of concurrent kernels (measured on MI355X: with 3 MB moved per step,
-// 8 entries per workgroup in flight on 64 workgroups stretch a concurrent
-// block scan from 57 to 98 us, 2 entries to 88 us). The grid is therefore one
-// workgroup per two pairs, kept between kCopyWorkgroupsMin and
-// kCopyWorkgroupsMax, with 2 entries in flight per workgroup (1 per batch;
-// more on small grids, so that the link still fills). Keeping the second
-// batch in flight while the first is stored raised the reasoning loop of
-// 32 layers x 64 requests from 6,300 to 6,710 tokens/s (the transfer there
-// paces the step) and changed 8 x 131,072 tokens by -1 %. Step rates measured
-// before that change (steps/s) for
-// 32 / 48 / 64 workgroups: 8 x 131,072 tokens (64 pairs) 10,490 / 9,790 /
-// 9,290; 32 requests of 16K-32K tokens (256 pairs) 7,920 / 8,540 / 8,400;
-// 16 x 65,536 tokens with B = 32 (128 pairs) 3,510 / 3,510 / 3,700. Fewer
-// workgroups mean more plans in series per workgroup, which the last two
-// cannot afford.
+// each workgroup keeps a batch of entries in flight. A plan costs a few
+// dependent global reads and a dozen barriers, so the pairs of a workgroup
+// are planned in one pass rather than one after another (measured on MI355X,
+// 8 x 131,072 tokens, 2 pairs per workgroup: the plans alone take 25 us of
+// an 80 us capped step when made in series; planned together, the step rate
+// rose from 10,350 to 10,660 steps/s).
+//
+// Host reads beyond what saturates the link only queue inside the GPU, where
+// they slow the HBM traffic of concurrent kernels (measured on MI355X: with
+// 3 MB moved per step, 8 entries per workgroup in flight on 64 workgroups
+// stretch a concurrent block scan from 57 to 98 us, 2 entries to 88 us). The
+// grid is therefore small, with 2 entries in flight per workgroup (1 per
+// batch; more on small grids, so that the link still fills): 32 workgroups at
+// B = 16; at B = 32, whose 16 KiB entries take twice the stores and
+// transposes, one per two pairs within 32 to 64. Step rates measured with
+// batched plans, 32 against 64 workgroups: 32 requests of 16K-32K tokens
+// (256 pairs) 9,020 against 8,220 steps/s; the reasoning loop of 32 layers x
+// 64 requests (512 pairs) 3,360 against 3,180 layer-steps/s; 16 x 65,536
+// tokens with B = 32 (128 pairs, paced by the transfer) 3,570 against 3,770.
+// Fewer than 32 (16, 8) were slower at 8 x 131,072 tokens. Keeping the second
+// batch in flight while the first is stored raised the reasoning loop from
+// 6,300 to 6,710 tokens/s and changed 8 x 131,072 tokens by -1 %.
 #include <climits>
 
 #include "oasis_internal.h"
@@ -51,9 +58,8 @@ namespace {
 constexpr int kPlanThreads = 256;
 constexpr int kMaxK = 1024;
 constexpr int kPer = kMaxK / kPlanThreads;  // items per thread in the scans
-constexpr int kKeyPad = 4;
-constexpr int kCopyWorkgroupsMin = 32;
-constexpr int kCopyWorkgroupsMax = 64;
+constexpr int kMaxPairs = 64;  // (request, KV head) pairs planned in one pass, at most
+constexpr int kCopyWorkgroups = 32;
 constexpr int kCopyInflightMin = 64;  // block-head entries (K and V) in flight over the whole grid, at least
 constexpr int kLocalWorkgroups = 256;  // grid of a local-block-only call
 
@@ -85,32 +91,36 @@ __device__ int wg_exclusive_scan(int v, int* s_wave) {
   return base + x - v;
 }
 
-// Plan of one (request, KV head); returns the number of entries in s_slot/s_page.
+// Plans of np (request, KV head) pairs, pair0 + p * stride for p < np, made
+// together (np * k <= kMaxK): item i of the pass is selection index and slot
+// i % k of pair p = i / k. Returns the number of entries written to
+// s_slot / s_page / s_epair (slot within the pair, host page, pair of the pass,
+// in ascending block id per pair); s_prh[p] receives the pair index of p.
 //
-// Misses and stale slots are first compacted (in ascending selection index and
-// ascending slot, which is ascending block id and slot order); each thread then
-// ranks one compacted item against all others, reading the keys four at a time
-// from LDS, so no thread walks a long chain of dependent reads.
-__device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int* s_page, int* s_wave) {
+// Misses, free slots and stale slots are compacted over the whole pass by
+// workgroup scans (in item order, so each pair's items form one contiguous
+// run in ascending block id or slot order); each thread then ranks one
+// compacted item against the others of its pair (misses by score under a cap,
+// stale slots by (stamp, slot)). Planning the pairs of a workgroup in one pass
+// pays the dependent global reads and the barriers once, not once per pair.
+__device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int* s_slot, int* s_page, int* s_epair,
+                         int* s_prh, int* s_wave) {
   const int tid = threadIdx.x;
   const int k = a.k;
-  // by selection index: s_sel, s_hit; by slot: s_map, s_stamp, s_keep; victims in order: s_vict;
-  // compacted misses: key, selection index, admitted; compacted stale slots: stamp, slot
-  __shared__ int s_sel[kMaxK], s_hit[kMaxK], s_map[kMaxK], s_stamp[kMaxK], s_keep[kMaxK], s_vict[kMaxK];
-  __shared__ __align__(16) unsigned s_mkey[kMaxK + kKeyPad];
-  __shared__ __align__(16) int s_skey[kMaxK + kKeyPad];
-  __shared__ int s_midx[kMaxK], s_madm[kMaxK], s_sslot[kMaxK];
-  // by selection index: the page of the block and its score key (under a possible cap)
+  const int N = np * k;
+  // by item: s_sel, s_hit (selection side), s_map, s_stamp, s_keep (slot side), s_selpage, s_selkey;
+  // compacted misses: key, item, admitted; compacted stale slots: stamp, item; ranked stale items; free items
+  __shared__ int s_sel[kMaxK], s_hit[kMaxK], s_map[kMaxK], s_stamp[kMaxK], s_keep[kMaxK];
   __shared__ int s_selpage[kMaxK];
-  __shared__ unsigned s_selkey[kMaxK];
+  __shared__ unsigned s_selkey[kMaxK], s_mkey[kMaxK];
+  __shared__ int s_midx[kMaxK], s_madm[kMaxK], s_skey[kMaxK], s_sslot[kMaxK], s_vstale[kMaxK], s_free[kMaxK];
+  // per pair: selected count, run starts of misses / free / stale items (np + 1 entries), admitted start, moved
+  __shared__ int s_pm[kMaxPairs], s_mstart[kMaxPairs + 1], s_fstart[kMaxPairs + 1], s_sstart[kMaxPairs + 1];
+  __shared__ int s_astart[kMaxPairs], s_moved[kMaxPairs];
 
-  const long long base = (long long)rh * k;
-  int m = a.sel_count[rh];
-  m = m < 0 ? 0 : (m > k ? k : m);
   // The page of every selected block (and, when a cap may bind, its score) is
   // fetched as soon as the block id arrives, so that these dependent loads
   // overlap the search below instead of stalling the pairing later.
-  const bool may_cap = a.fetch_cap < m;
   int pg[kPer];
   unsigned ky[kPer];
 #pragma unroll
@@ -118,34 +128,49 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
     const int i = tid + j * kPlanThreads;
     pg[j] = -1;
     ky[j] = 0u;
-    if (i < k) {
-      const int sv = a.sel[base + i];  // in the row (k entries); loaded without waiting for the count
-      const int b = i < m ? sv : INT_MAX;
+    if (i < N) {
+      const int p = i / k;
+      const int li = i - p * k;
+      const int rh = pair0 + p * stride;
+      const long long row = (long long)rh * k;
+      const int sv = a.sel[row + li];  // in the row (k entries); loaded without waiting for the count
+      int m = a.sel_count[rh];
+      m = m < 0 ? 0 : (m > k ? k : m);
+      const int b = li < m ? sv : INT_MAX;
       s_sel[i] = b;
       s_hit[i] = 0;
-      s_map[i] = a.slot_map[base + i];
-      s_stamp[i] = a.slot_stamp[base + i];
-      if (i < m) {
+      s_map[i] = a.slot_map[row + li];
+      s_stamp[i] = a.slot_stamp[row + li];
+      if (li == 0) {
+        s_pm[p] = m;
+        s_prh[p] = rh;
+        s_moved[p] = 0;
+      }
+      if (li < m) {
+        const int r = rh / a.Hkv;
         const bool in_row = b >= 0 && b < a.NBmax;
         if (in_row) pg[j] = a.block_table[(long long)r * a.NBmax + b];
-        if (may_cap) ky[j] = order_key(in_row ? a.scores[(long long)rh * a.NBmax + b] : -__builtin_inff());
+        if (a.fetch_cap < m) ky[j] = order_key(in_row ? a.scores[(long long)rh * a.NBmax + b] : -__builtin_inff());
       }
     }
   }
   __syncthreads();
 
-  // resident hits: binary search of every resident block in the (ascending) selection
-  for (int s = tid; s < k; s += kPlanThreads) {
+  // resident hits: binary search of every resident block in its pair's (ascending) selection
+  for (int s = tid; s < N; s += kPlanThreads) {
+    const int p = s / k;
+    const int off = p * k;
+    const int m = s_pm[p];
     const int b = s_map[s];
     int keep = 0;
     if (b >= 0) {
       int lo = 0, hi = m;
       while (lo < hi) {
         const int mid = (lo + hi) >> 1;
-        if (s_sel[mid] < b) lo = mid + 1; else hi = mid;
+        if (s_sel[off + mid] < b) lo = mid + 1; else hi = mid;
       }
-      if (lo < m && s_sel[lo] == b) {
-        s_hit[lo] = 1;
+      if (lo < m && s_sel[off + lo] == b) {
+        s_hit[off + lo] = 1;
         keep = 1;
       }
     }
@@ -154,21 +179,22 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     const int i = tid + j * kPlanThreads;
-    if (i < k) {
+    if (i < N) {
       s_selpage[i] = pg[j];
       s_selkey[i] = ky[j];
     }
   }
   __syncthreads();
 
-  // items [i0, i0 + kPer): selection entries (misses) and slots (free, stale)
+  // items [i0, i0 + kPer): misses (selection side), free and stale slots (slot side)
   const int i0 = tid * kPer;
   int nm = 0, nf = 0, ns = 0;
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
     const int i = i0 + j;
-    if (i < m && !s_hit[i]) ++nm;
-    if (i < k) {
+    if (i < N) {
+      const int p = i / k;
+      if (i - p * k < s_pm[p] && !s_hit[i]) ++nm;
       if (s_map[i] < 0) ++nf;
       else if (!s_keep[i]) ++ns;
     }
@@ -179,25 +205,26 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
   const int n_stale = s_wave[4];
   const int n_miss = mf_tot & 0xFFFF;
   const int n_free = mf_tot >> 16;
-
-  // admission: every miss, or under a binding cap the fetch_cap misses with the
-  // highest score (ties: lowest block id). Keys are order-preserving integers, so
-  // the ranks are distinct even for NaN scores and exactly fetch_cap misses are
-  // admitted.
-  const bool capped = a.fetch_cap < n_miss;
   {
     int mr = mf_base & 0xFFFF, fr = mf_base >> 16, sr = st_base;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int i = i0 + j;
-      if (i < m && !s_hit[i]) {
-        s_mkey[mr] = capped ? s_selkey[i] : 0u;
-        s_midx[mr] = i;
-        ++mr;
-      }
-      if (i < k) {
+      if (i < N) {
+        const int p = i / k;
+        const int li = i - p * k;
+        if (li == 0) {  // the pair's runs start here
+          s_mstart[p] = mr;
+          s_fstart[p] = fr;
+          s_sstart[p] = sr;
+        }
+        if (li < s_pm[p] && !s_hit[i]) {
+          s_mkey[mr] = s_selkey[i];
+          s_midx[mr] = i;
+          ++mr;
+        }
         if (s_map[i] < 0) {
-          s_vict[fr++] = i;
+          s_free[fr++] = i;
         } else if (!s_keep[i]) {
           s_skey[sr] = s_stamp[i];
           s_sslot[sr] = i;
@@ -205,46 +232,50 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
         }
       }
     }
-    // pads read by the 4-wide loops below; they never rank ahead of a real item
-    if (tid < kKeyPad) {
-      s_mkey[n_miss + tid] = 0u;
-      s_skey[n_stale + tid] = INT_MAX;
+    if (tid == 0) {
+      s_mstart[np] = n_miss;
+      s_fstart[np] = n_free;
+      s_sstart[np] = n_stale;
     }
   }
   __syncthreads();
 
+  // admission: every miss of a pair, or under a binding cap its fetch_cap misses
+  // with the highest score (ties: lowest block id). Keys are order-preserving
+  // integers, so the ranks are distinct even for NaN scores and exactly
+  // fetch_cap misses are admitted.
   for (int c = tid; c < n_miss; c += kPlanThreads) {
+    const int p = s_midx[c] / k;
+    const int ms = s_mstart[p], me = s_mstart[p + 1];
     int adm = 1;
-    if (capped) {
+    if (a.fetch_cap < me - ms) {
       const unsigned key = s_mkey[c];
       int rank = 0;
 #pragma unroll 4
-      for (int t = 0; t < n_miss; t += 4) {
-        const u32x4 kt = *reinterpret_cast<const u32x4*>(&s_mkey[t]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) rank += (kt[e] > key) || (kt[e] == key && t + e < c);
+      for (int t = ms; t < me; ++t) {
+        const unsigned kt = s_mkey[t];
+        rank += (kt > key) || (kt == key && t < c);
       }
       adm = rank < a.fetch_cap;
     }
     s_madm[c] = adm;
   }
-  // victim order: free slots ascending (already in s_vict), then stale slots by (stamp, slot)
+  // victim order per pair: free slots ascending (s_free), then stale slots by (stamp, slot)
   for (int c = tid; c < n_stale; c += kPlanThreads) {
+    const int p = s_sslot[c] / k;
+    const int ss = s_sstart[p], se = s_sstart[p + 1];
     const int st = s_skey[c];
     int rank = 0;
 #pragma unroll 4
-    for (int t = 0; t < n_stale; t += 4) {
-      const int4 kt = *reinterpret_cast<const int4*>(&s_skey[t]);
-      rank += (kt.x < st) || (kt.x == st && t < c);
-      rank += (kt.y < st) || (kt.y == st && t + 1 < c);
-      rank += (kt.z < st) || (kt.z == st && t + 2 < c);
-      rank += (kt.w < st) || (kt.w == st && t + 3 < c);
+    for (int t = ss; t < se; ++t) {
+      const int kt = s_skey[t];
+      rank += (kt < st) || (kt == st && t < c);
     }
-    s_vict[n_free + rank] = s_sslot[c];
+    s_vstale[ss + rank] = s_sslot[c];
   }
   __syncthreads();
 
-  // the i-th admitted miss (ascending block id) goes to the i-th victim
+  // the a-th admitted miss of a pair (ascending block id) goes to its a-th victim
   int na = 0;
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
@@ -253,37 +284,56 @@ __device__ int plan_entries(const StageArgs& a, int rh, int r, int* s_slot, int*
   }
   const int adm_base = wg_exclusive_scan(na, s_wave);
   const int n_adm = s_wave[4];
-  const int n_vict = n_free + n_stale;
-  int moved_local = 0;
+  {
+    int ar = adm_base;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int c = i0 + j;
+      if (c < n_miss) {
+        const int p = s_midx[c] / k;
+        if (c == s_mstart[p]) s_astart[p] = ar;  // admitted misses of the pairs before p
+        ar += s_madm[c];
+      }
+    }
+  }
+  __syncthreads();
   {
     int ar = adm_base;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const int c = i0 + j;
       if (c >= n_miss || !s_madm[c]) continue;
+      const int i = s_midx[c];
+      const int p = i / k;
+      const int rank = ar - s_astart[p];
+      const int f0 = s_fstart[p], nfp = s_fstart[p + 1] - f0;
+      const int s0 = s_sstart[p], nsp = s_sstart[p + 1] - s0;
       // a slot map holding one block twice can leave fewer victims than misses
-      const int v = ar < n_vict ? s_vict[ar] : -1;
-      const int blk = s_sel[s_midx[c]];
-      int page = v >= 0 ? s_selpage[s_midx[c]] : -1;
+      const int v = rank < nfp ? s_free[f0 + rank] : (rank < nfp + nsp ? s_vstale[s0 + rank - nfp] : -1);
+      const int blk = s_sel[i];
+      int page = v >= 0 ? s_selpage[i] : -1;
       if (page < 0 || page >= a.num_pages) page = -1;
-      s_slot[ar] = v;
+      s_slot[ar] = v >= 0 ? v - p * k : -1;
       s_page[ar] = page;
+      s_epair[ar] = p;
       if (v >= 0) {
         s_map[v] = page >= 0 ? blk : -1;
         s_keep[v] = page >= 0;
       }
-      moved_local += page >= 0;
+      if (page >= 0) atomicAdd(&s_moved[p], 1);
       ++ar;
     }
   }
-  wg_exclusive_scan(moved_local, s_wave);
-  const int moved = s_wave[4];
+  __syncthreads();
 
-  for (int s = tid; s < k; s += kPlanThreads) {
-    a.slot_map[base + s] = s_map[s];
-    if (s_keep[s]) a.slot_stamp[base + s] = a.step;
+  for (int s = tid; s < N; s += kPlanThreads) {
+    const int p = s / k;
+    const long long at = (long long)s_prh[p] * k + (s - p * k);
+    a.slot_map[at] = s_map[s];
+    if (s_keep[s]) a.slot_stamp[at] = a.step;
   }
-  if (tid == 0 && a.moved) a.moved[rh] = moved;
+  if (a.moved)
+    for (int p = tid; p < np; p += kPlanThreads) a.moved[s_prh[p]] = s_moved[p];
   return n_adm;
 }
 
@@ -293,26 +343,28 @@ template <int BS, int PF>
 struct CopyBatch {
   static constexpr int kChunks = BS * kHeadDim / 8 / kPlanThreads;
   u32x4 k[PF][kChunks], v[PF][kChunks];
-  int slot[PF], page[PF];
+  int rh[PF], slot[PF], page[PF];
 };
 
 template <int BS, int PF>
-__device__ __forceinline__ void fetch_batch(const StageArgs& a, CopyBatch<BS, PF>& b, int e0, int n, int r, int h,
-                                            const int* s_slot, const int* s_page) {
+__device__ __forceinline__ void fetch_batch(const StageArgs& a, CopyBatch<BS, PF>& b, int e0, int n,
+                                            const int* s_slot, const int* s_page, const int* s_epair,
+                                            const int* s_prh) {
   constexpr int kElems = BS * kHeadDim;
   const int tid = threadIdx.x;
-  // placeholder source: slot 0 of this (r, h) in the pool
-  const long long hold = (((long long)r * (a.k + 1)) * a.Hkv + h) * kElems;
 #pragma unroll
   for (int p = 0; p < PF; ++p) {
     const int e = e0 + p;
     b.slot[p] = e < n ? s_slot[e] : -1;
     b.page[p] = e < n ? s_page[e] : -1;
+    b.rh[p] = e < n ? s_prh[s_epair[e]] : 0;
     const bool live = b.page[p] >= 0 && b.slot[p] >= 0 && b.slot[p] <= a.k;
     if (!live) b.page[p] = -1;
+    const int h = b.rh[p] % a.Hkv;
     const long long src = ((long long)(live ? b.page[p] : 0) * a.Hkv + h) * kElems;
-    const uint16_t* ks = live ? a.host_k + src : a.pool_k + hold;
-    const uint16_t* vs = live ? a.host_v + src : a.pool_k + hold;
+    // placeholder source (no entry): the start of the pool (device memory, discarded)
+    const uint16_t* ks = live ? a.host_k + src : a.pool_k;
+    const uint16_t* vs = live ? a.host_v + src : a.pool_k;
 #pragma unroll
     for (int q = 0; q < CopyBatch<BS, PF>::kChunks; ++q) {
       const int c = (q * kPlanThreads + tid) * 8;
@@ -325,18 +377,24 @@ __device__ __forceinline__ void fetch_batch(const StageArgs& a, CopyBatch<BS, PF
 // Store a fetched batch: K token-major into the pool, V transposed through LDS
 // into the d x B layout the attention kernel reads.
 template <int BS, int PF>
-__device__ __forceinline__ void put_batch(const StageArgs& a, const CopyBatch<BS, PF>& b, int r, int h,
+__device__ __forceinline__ void put_batch(const StageArgs& a, const CopyBatch<BS, PF>& b,
                                           uint16_t (*tile)[BS * kHeadDim]) {
   constexpr int kElems = BS * kHeadDim;
   const int tid = threadIdx.x;
+  long long dst[PF];
+#pragma unroll
+  for (int p = 0; p < PF; ++p) {
+    const int r = b.rh[p] / a.Hkv;
+    const int h = b.rh[p] - r * a.Hkv;
+    dst[p] = (((long long)r * (a.k + 1) + b.slot[p]) * a.Hkv + h) * kElems;
+  }
 #pragma unroll
   for (int p = 0; p < PF; ++p) {
     if (b.page[p] < 0) continue;
-    const long long dst = (((long long)r * (a.k + 1) + b.slot[p]) * a.Hkv + h) * kElems;
 #pragma unroll
     for (int q = 0; q < CopyBatch<BS, PF>::kChunks; ++q) {
       const int c = (q * kPlanThreads + tid) * 8;
-      *reinterpret_cast<u32x4*>(a.pool_k + dst + c) = b.k[p][q];
+      *reinterpret_cast<u32x4*>(a.pool_k + dst[p] + c) = b.k[p][q];
       *reinterpret_cast<u32x4*>(&tile[p][c]) = b.v[p][q];
     }
   }
@@ -346,7 +404,6 @@ __device__ __forceinline__ void put_batch(const StageArgs& a, const CopyBatch<BS
 #pragma unroll
   for (int p = 0; p < PF; ++p) {
     if (b.page[p] < 0) continue;
-    const long long dst = (((long long)r * (a.k + 1) + b.slot[p]) * a.Hkv + h) * kElems;
 #pragma unroll
     for (int w = tid; w < kHeadDim * kGroups; w += kPlanThreads) {
       const int d = w / kGroups;
@@ -358,52 +415,73 @@ __device__ __forceinline__ void put_batch(const StageArgs& a, const CopyBatch<BS
         const uint32_t hi = tile[p][(t0 + 2 * j + 1) * kHeadDim + d];
         o[j] = lo | (hi << 16);
       }
-      *reinterpret_cast<u32x4*>(a.pool_v + dst + (long long)d * BS + t0) = o;
+      *reinterpret_cast<u32x4*>(a.pool_v + dst[p] + (long long)d * BS + t0) = o;
     }
   }
   __syncthreads();
 }
 
+template <int BS, int PF, int TP>
+__device__ __forceinline__ void copy_entries(const StageArgs& a, int n, const int* s_slot, const int* s_page,
+                                             const int* s_epair, const int* s_prh, uint16_t (*tile)[TP]) {
+  CopyBatch<BS, PF> x, y;
+  fetch_batch<BS, PF>(a, x, 0, n, s_slot, s_page, s_epair, s_prh);
+  for (int e0 = 0; e0 < n; e0 += 2 * PF) {
+    fetch_batch<BS, PF>(a, y, e0 + PF, n, s_slot, s_page, s_epair, s_prh);
+    put_batch<BS, PF>(a, x, tile);
+    if (e0 + PF >= n) break;
+    fetch_batch<BS, PF>(a, x, e0 + 2 * PF, n, s_slot, s_page, s_epair, s_prh);
+    put_batch<BS, PF>(a, y, tile);
+  }
+}
+
 template <int BS, int PF>
 __global__ __launch_bounds__(kPlanThreads) void stage_kernel(StageArgs a) {
   const int tid = threadIdx.x;
-  __shared__ int s_slot[kMaxK + 1], s_page[kMaxK + 1];
+  __shared__ int s_slot[kMaxK + kMaxPairs], s_page[kMaxK + kMaxPairs], s_epair[kMaxK + kMaxPairs];
+  __shared__ int s_prh[kMaxPairs];
   __shared__ int s_wave[8];
-  constexpr int kElems = BS * kHeadDim;          // one K (or V) block-head entry
+  constexpr int kElems = BS * kHeadDim;  // one K (or V) block-head entry
   __shared__ uint16_t tile[PF][kElems];
 
-  for (int rh = blockIdx.x; rh < a.R * a.Hkv; rh += gridDim.x) {
-  const int r = rh / a.Hkv;
-  const int h = rh - r * a.Hkv;
-  int n = a.local_only ? 0 : plan_entries(a, rh, r, s_slot, s_page, s_wave);
-  if (a.copy_local) {
-    const Ctx c = ctx_blocks(a.ctx_len[r], BS, a.NBmax);
-    if (c.nb > 0) {
-      const int page = a.block_table[(long long)r * a.NBmax + c.nb - 1];
-      if (tid == 0) {
-        s_slot[n] = a.k;
-        s_page[n] = (page >= 0 && page < a.num_pages) ? page : -1;
-      }
-      ++n;
+  // this workgroup's pairs: blockIdx.x, blockIdx.x + gridDim.x, ...; up to
+  // kMaxK / k of them (kMaxPairs at most) are planned and copied per pass
+  const int nrh = a.R * a.Hkv;
+  const int stride = gridDim.x;
+  const int mine = (int)blockIdx.x < nrh ? (nrh - 1 - (int)blockIdx.x) / stride + 1 : 0;
+  int per_pass = a.local_only ? kMaxPairs : kMaxK / a.k;
+  per_pass = per_pass < 1 ? 1 : (per_pass > kMaxPairs ? kMaxPairs : per_pass);
+  for (int j0 = 0; j0 < mine; j0 += per_pass) {
+    const int np = mine - j0 < per_pass ? mine - j0 : per_pass;
+    const int pair0 = (int)blockIdx.x + j0 * stride;
+    int n = 0;
+    if (a.local_only) {
+      for (int p = tid; p < np; p += kPlanThreads) s_prh[p] = pair0 + p * stride;
+    } else {
+      n = plan_pass(a, pair0, np, stride, s_slot, s_page, s_epair, s_prh, s_wave);
     }
-  }
-  __syncthreads();
+    if (a.copy_local) {  // the local block of every pair of the pass, into slot k
+      for (int p = tid; p < np; p += kPlanThreads) {
+        const int rh = pair0 + p * stride;
+        const int r = rh / a.Hkv;
+        const Ctx c = ctx_blocks(a.ctx_len[r], BS, a.NBmax);
+        int page = c.nb > 0 ? a.block_table[(long long)r * a.NBmax + c.nb - 1] : -1;
+        if (page < 0 || page >= a.num_pages) page = -1;
+        s_slot[n + p] = a.k;
+        s_page[n + p] = page;
+        s_epair[n + p] = p;
+      }
+      n += np;
+    }
+    __syncthreads();
 
-  // Batches of PF entries, two in flight: the host reads of the next batch are
-  // issued before the current one is stored, so the link does not idle while
-  // a batch is written and V is transposed. Every load is issued; an entry
-  // past the end (or without a page) reads slot 0 of this (r, h) in the pool
-  // instead (device memory, discarded), so the wait counts stay exact.
-  CopyBatch<BS, PF> x, y;
-  fetch_batch<BS, PF>(a, x, 0, n, r, h, s_slot, s_page);
-  for (int e0 = 0; e0 < n; e0 += 2 * PF) {
-    fetch_batch<BS, PF>(a, y, e0 + PF, n, r, h, s_slot, s_page);
-    put_batch<BS, PF>(a, x, r, h, tile);
-    if (e0 + PF >= n) break;
-    fetch_batch<BS, PF>(a, x, e0 + 2 * PF, n, r, h, s_slot, s_page);
-    put_batch<BS, PF>(a, y, r, h, tile);
-  }
-  __syncthreads();  // LDS plan arrays are reused by the next pair
+    // Batches of PF entries, two in flight: the host reads of the next batch
+    // are issued before the current one is stored, so the link does not idle
+    // while a batch is written and V is transposed. Every load is issued; an
+    // entry past the end (or without a page) reads the start of the pool
+    // instead (device memory, discarded), so the wait counts stay exact.
+    copy_entries<BS, PF>(a, n, s_slot, s_page, s_epair, s_prh, tile);
+    __syncthreads();  // LDS plan arrays are reused by the next pass
   }
 }
 
@@ -413,8 +491,10 @@ template <int BS>
 hipError_t launch_bs(const StageArgs& a, hipStream_t s, const LaunchTiming& t) {
   const int nrh = a.R * a.Hkv;
   if (nrh <= 0) return hipSuccess;
-  int grid = nrh / 2;
-  grid = grid < kCopyWorkgroupsMin ? kCopyWorkgroupsMin : (grid > kCopyWorkgroupsMax ? kCopyWorkgroupsMax : grid);
+  // B = 16: kCopyWorkgroups; B = 32 (16 KiB entries, twice the stores and
+  // transposes per entry): one workgroup per two pairs, up to twice as many
+  int grid = BS == 16 ? kCopyWorkgroups : nrh / 2;
+  grid = grid < kCopyWorkgroups ? kCopyWorkgroups : (grid > 2 * kCopyWorkgroups ? 2 * kCopyWorkgroups : grid);
   // the local block alone (no plan, one entry per pair, on the caller's critical path): spread wide
   if (a.local_only) grid = nrh < kLocalWorkgroups ? nrh : kLocalWorkgroups;
   if (grid > nrh) grid = nrh;

@@ -261,6 +261,57 @@ def test_stage_capped_exact(case, cap):
         assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv), step
 
 
+STAGE_PASS_CASES = [
+    # (seed, requests, k, fetch cap or None, context range): (request, KV head) pairs per staging
+    # workgroup and per plan pass (a pass holds up to 1024 / k pairs, 64 at most)
+    (1, 40, 100, None, (200, 2400)),   # 320 pairs: 5 per workgroup, planned in one pass of 500 items
+    (2, 40, 300, 7, (1, 5200)),        # 3 pairs per pass: passes of 3 and 2, capped
+    (3, 40, 13, 2, (1, 400)),          # k not a multiple of 4, capped
+    (4, 64, 128, 6, (1000, 2600)),     # 8 pairs per workgroup: one full pass of 1024 items
+    (5, 600, 3, None, (1, 90)),        # 75 pairs per workgroup: passes of 64 and 11
+]
+
+
+@pytest.mark.parametrize("seed,R,k,cap,ctx_args", STAGE_PASS_CASES)
+def test_stage_many_pairs_exact(seed, R, k, cap, ctx_args):
+    """Several (request, KV head) plans per workgroup pass: slot maps, stamps, counts and bytes bit-exact."""
+    w = make_workload("c2", num_reqs=R, ctx_args=ctx_args, budget=16 * k)
+    c = w.cfg
+    hk_t, hv_t = pinned_pages(w)
+    d = _dims(w)
+    ctx = w.ctx_len(0)
+    n_cand = np.array([O.block_counts(L, c.block_size)[1] for L in ctx])
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap if cap else k)
+    st = LayerState(d, c.T, k)
+    hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
+    smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
+    stamp = np.zeros_like(smap)
+    pk = np.zeros((c.num_reqs, k + 1, c.num_kv_heads, c.block_size, c.head_dim), np.uint16)
+    pv = np.zeros_like(pk)
+    sel, cnt = random_selection_h(700 + seed, n_cand, c.num_kv_heads, k)
+    ctx_d = dev_i32(ctx)
+    for step in range(1, 4):
+        if step > 1:
+            sel, cnt = random_selection(700 + seed + step, n_cand, k, prev=(sel, cnt), keep_frac=0.7)
+        scores = random_scores(750 + seed + step, (c.num_reqs, c.num_kv_heads, w.NBmax),
+                               n_distinct=9 if step == 2 else None)
+        moved = O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, step, pk, pv, ctx, c.block_size,
+                               copy_local=True, scores=scores, fetch_cap=cap if cap else k)
+        note(f"stage many pairs seed={seed} R={R} k={k} cap={cap} step={step}")
+        st.sel.copy_(torch.from_numpy(sel))
+        st.sel_count.copy_(torch.from_numpy(cnt))
+        st.scores.copy_(torch.from_numpy(scores))
+        path.stage(st, ctx_d, step)
+        torch.cuda.synchronize()
+        assert np.array_equal(st.slot_map.cpu().numpy(), smap), step
+        assert np.array_equal(st.slot_stamp.cpu().numpy(), stamp), step
+        assert np.array_equal(st.moved.cpu().numpy(), moved), step
+        if cap:
+            assert moved.max(initial=0) <= cap
+        assert np.array_equal(host_bits(st.pool_k), pk), step
+        assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv), step
+
+
 def test_stage_local_only(case):
     name, w, hk_t, hv_t = case
     c = w.cfg

@@ -269,6 +269,7 @@ STAGE_PASS_CASES = [
     (3, 40, 13, 2, (1, 400)),          # k not a multiple of 4, capped
     (4, 64, 128, 6, (1000, 2600)),     # 8 pairs per workgroup: one full pass of 1024 items
     (5, 600, 3, None, (1, 90)),        # 75 pairs per workgroup: passes of 64 and 11
+    (6, 5, 1024, 40, (100, 20000)),    # k = 1024: one pair per pass, two passes on some workgroups
 ]
 
 
@@ -310,6 +311,20 @@ def test_stage_many_pairs_exact(seed, R, k, cap, ctx_args):
             assert moved.max(initial=0) <= cap
         assert np.array_equal(host_bits(st.pool_k), pk), step
         assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv), step
+    # the local blocks alone (no plan; up to 256 workgroups, several pairs each beyond 256 pairs)
+    st.pool_k[:, k].zero_()
+    st.pool_v[:, k].zero_()
+    pk[:, k] = 0
+    pv[:, k] = 0
+    note(f"stage many pairs local-only seed={seed} R={R} k={k}")
+    path.refresh_local(st, ctx_d)
+    torch.cuda.synchronize()
+    smap_before = smap.copy()
+    O.stage_blocks(hk, hv, w.block_table, np.full_like(smap, -1), np.zeros_like(cnt), smap.copy(), stamp.copy(),
+                   0, pk, pv, ctx, c.block_size, copy_local=True)
+    assert np.array_equal(host_bits(st.pool_k), pk)
+    assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv)
+    assert np.array_equal(st.slot_map.cpu().numpy(), smap_before)
 
 
 def test_stage_local_only(case):

@@ -17,107 +17,27 @@
 // read 64 contiguous bytes and the wave covers the tile's 2 x 4 KiB in 8
 // load instructions. All loads of a wave are issued before its first MFMA.
 //
-// One row tile (up to 16 rows): every wave keeps the [q+ | q-] operands in
-// registers next to 4 summary tiles. Two to four row tiles: the operands go
-// to LDS once per workgroup and waves walk the row tiles in an outer loop
-// (score_kernel_lds), so a wave holds one row tile's operands; measured on
-// MI355X at 64 rows (16 requests x 65,536 tokens, B = 32, 134 MB): 30.1 us
-// against 38.5 us with all operands in every wave's registers (2 waves per
-// SIMD there, 4 here).
+// The operands of the rows go to LDS once per workgroup and each wave holds
+// one row tile's operands at a time (4 summary tiles per wave with one row
+// tile, 2 with more). Measured on MI355X against keeping all operands in
+// every wave's registers: 64 rows (16 requests x 65,536 tokens, B = 32,
+// 134 MB) 30.1 us against 38.5 us (4 waves per SIMD instead of 2); 16 rows
+// (8 x 131,072 tokens, 268 MB) 48.6 us against 49.9 us (fewer query reads;
+// 3, 5, 6 and 8 summary tiles per wave: 48.6, 50.8, 51.7 and 56.6 us).
 #include "oasis_internal.h"
 
 namespace oasis {
 
 namespace {
 
+// The [q+ | q-] operands of the KV head's rows are built once per workgroup in
+// LDS, laid out per lane so that each MFMA operand is one conflict-free
+// 16-byte LDS read, and a wave walks the row tiles in its outer loop. Only one
+// row tile's operands are then live in registers, which leaves room for more
+// summary tiles in flight per CU, and the queries are read once per workgroup
+// rather than once per wave.
 template <int NRT, int TPW>
 __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
-  const int wave = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
-  const int g = lane >> 4;   // k-group of the MFMA operands
-  const int n = lane & 15;   // block within the tile (B operand) / row within the tile (A operand)
-  const int rh = blockIdx.y;
-  const int r = rh / a.Hkv;
-  const int h = rh - r * a.Hkv;
-  const Ctx c = ctx_blocks(a.ctx_len[r], a.B, a.NBmax);
-  const int ntiles = (a.NBmax + 15) >> 4;
-  const int tile0 = (blockIdx.x * 4 + wave) * TPW;
-  if (tile0 >= ntiles) return;
-
-  float* srow = a.scores + (long long)rh * a.NBmax;
-  const long long sum_base = (long long)rh * a.NBmax * kHeadDim;
-  const uint16_t* kmx = a.kmax + sum_base;
-  const uint16_t* kmn = a.kmin + sum_base;
-
-  // Issue the summary loads of all TPW tiles first.
-  u32x4 vmax[TPW][4], vmin[TPW][4];
-#pragma unroll
-  for (int t = 0; t < TPW; ++t) {
-    const int blk = (tile0 + t) * 16 + n;
-    const bool live = blk < c.n_cand;
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      const long long off = (long long)blk * kHeadDim + st * 32 + g * 8;
-      vmax[t][st] = live ? ldg16(kmx + off) : u32x4{0, 0, 0, 0};
-      vmin[t][st] = live ? ldg16(kmn + off) : u32x4{0, 0, 0, 0};
-    }
-  }
-
-  // A operands: [q+ | q-] of the rows of this KV head. Rows past the last
-  // real row repeat row 0, which leaves the maximum unchanged.
-  const int nrows = a.num_draft * a.G;
-  bf16x8 qpos[NRT][4], qneg[NRT][4];
-#pragma unroll
-  for (int v = 0; v < NRT; ++v) {
-    int row = v * 16 + n;
-    if (row >= nrows) row = 0;
-    const int t = a.first_draft + row / a.G;
-    const int qh = h * a.G + row % a.G;
-    const uint16_t* qrow = a.q + (((long long)r * a.T + t) * a.Hq + qh) * kHeadDim;
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      u32x4 p, m;
-      split_sign(ldg16(qrow + st * 32 + g * 8), p, m);
-      qpos[v][st] = as_bf16x8(p);
-      qneg[v][st] = as_bf16x8(m);
-    }
-  }
-
-#pragma unroll
-  for (int t = 0; t < TPW; ++t) {
-    const int tile = tile0 + t;
-    if (tile >= ntiles) break;
-    const int b0 = tile * 16;
-    float best = -INFINITY;
-    if (b0 < c.n_cand) {
-#pragma unroll
-      for (int v = 0; v < NRT; ++v) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qpos[v][st], as_bf16x8(vmax[t][st]), acc, 0, 0, 0);
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qneg[v][st], as_bf16x8(vmin[t][st]), acc, 0, 0, 0);
-        // lane (g, n) holds rows 4g..4g+3 of the row tile for block n
-        best = fmaxf(best, fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
-      }
-      best = fmaxf(best, __shfl_xor(best, 16));
-      best = fmaxf(best, __shfl_xor(best, 32));
-    }
-    const int blk = b0 + n;
-    if (g == 0 && blk < a.NBmax) srow[blk] = blk < c.n_cand ? best : -INFINITY;
-  }
-}
-
-// Many rows (two or more row tiles): the [q+ | q-] operands of the KV head's
-// rows are built once per workgroup in LDS, laid out per lane so that each
-// MFMA operand is one conflict-free 16-byte LDS read, and a wave walks the row
-// tiles in its outer loop. Only one row tile's operands are then live in
-// registers, which leaves room for more summary tiles in flight per CU than
-// holding every row tile's operands in every wave would.
-template <int NRT, int TPW>
-__global__ __launch_bounds__(256) void score_kernel_lds(ScoreArgs a) {
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
@@ -211,14 +131,6 @@ __global__ __launch_bounds__(256) void score_kernel_lds(ScoreArgs a) {
 }
 
 template <int NRT, int TPW>
-hipError_t launch_lds(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t) {
-  const int ntiles = (a.NBmax + 15) / 16;
-  const dim3 grid((unsigned)((ntiles + 4 * TPW - 1) / (4 * TPW)), (unsigned)(a.R * a.Hkv));
-  launch_kernel(score_kernel_lds<NRT, TPW>, grid, dim3(256), s, t, a);
-  return hipGetLastError();
-}
-
-template <int NRT, int TPW>
 hipError_t launch_t(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t) {
   const int ntiles = (a.NBmax + 15) / 16;
   const dim3 grid((unsigned)((ntiles + 4 * TPW - 1) / (4 * TPW)), (unsigned)(a.R * a.Hkv));
@@ -234,9 +146,9 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t
   if (rows <= kScoreValuMaxRows) return launch_score_valu(a, s, t);
   switch ((rows + 15) / 16) {
     case 1: return launch_t<1, 4>(a, s, t);
-    case 2: return launch_lds<2, 2>(a, s, t);
-    case 3: return launch_lds<3, 2>(a, s, t);
-    case 4: return launch_lds<4, 2>(a, s, t);
+    case 2: return launch_t<2, 2>(a, s, t);
+    case 3: return launch_t<3, 2>(a, s, t);
+    case 4: return launch_t<4, 2>(a, s, t);
     default: return hipErrorInvalidValue;
   }
 }

@@ -13,7 +13,7 @@ constexpr int kThreads = 1024;
 
 template <int KPT>
 __global__ __launch_bounds__(kThreads) void topk_kernel(TopkArgs a) {
-  __shared__ SelectShared<kThreads> sh;
+  __shared__ SelectShared<kThreads, KPT> sh;
   const int rh = blockIdx.x;
   const int r = rh / a.Hkv;
   const Ctx c = ctx_blocks(a.ctx_len[r], a.B, a.NBmax);

@@ -114,6 +114,19 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t
 constexpr int kScoreValuMaxRows = 4;
 hipError_t launch_score_valu(const ScoreArgs& a, hipStream_t s, const LaunchTiming& t = {});
 
+// Wave-wide inclusive prefix sum on the DPP network (no LDS round trips):
+// row shifts by 1, 2, 4 and 8 give each 16-lane row its own prefix sums, then
+// row broadcasts of lanes 15 and 31 carry the totals of the earlier rows.
+__device__ __forceinline__ int wave_incl_sum(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);  // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);  // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);  // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15 into rows 1 and 3
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
 // Split bf16 pairs into their non-negative and non-positive parts (bitwise, exact).
 __device__ __forceinline__ void split_sign(u32x4 v, u32x4& pos, u32x4& neg) {
 #pragma unroll

@@ -28,19 +28,6 @@ __device__ __forceinline__ uint32_t select_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Wave-wide inclusive prefix sum on the DPP network (no LDS round trips):
-// row shifts by 1, 2, 4 and 8 give each 16-lane row its own prefix sums, then
-// row broadcasts of lanes 15 and 31 carry the totals of the earlier rows.
-__device__ __forceinline__ int wave_incl_sum(int x) {
-  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);  // row_shr:1
-  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);  // row_shr:2
-  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);  // row_shr:4
-  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);  // row_shr:8
-  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);  // row_bcast:15 into rows 1 and 3
-  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);  // row_bcast:31 into rows 2 and 3
-  return x;
-}
-
 // Wave-wide minimum and maximum of uint32 values, returned to every lane (the
 // same DPP steps; lanes without a source keep the identity).
 __device__ __forceinline__ void wave_min_max(uint32_t& mn, uint32_t& mx) {

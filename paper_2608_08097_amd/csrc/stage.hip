@@ -73,12 +73,7 @@ __device__ inline unsigned order_key(float f) {
 __device__ int wg_exclusive_scan(int v, int* s_wave) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  int x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
+  const int x = wave_incl_sum(v);
   if (lane == 63) s_wave[wave] = x;
   __syncthreads();
   int base = 0;

@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define OASIS_ABI_VERSION 4
+#define OASIS_ABI_VERSION 5
 
 /* Only the entry points below are exported from liboasis.so. */
 #if defined(__GNUC__) || defined(__clang__)
@@ -354,6 +354,22 @@ OASIS_API oasis_status oasis_pipeline_set_layer(oasis_pipeline* pipeline, int32_
 OASIS_API oasis_status oasis_pipeline_set_local_source(oasis_pipeline* pipeline, const uint16_t* k_pages,
                                              const uint16_t* v_pages, int64_t num_pages,
                                              const int32_t* block_table);
+
+/* Where a step plans its transfer (paper §4.2.3, the delta selection between the
+ * prediction and the transfer of §4.2.2). OASIS_PLAN_ON_TRANSFER (the default):
+ * the staging kernel on the transfer stream plans and then copies.
+ * OASIS_PLAN_ON_PREDICTION: the top-K kernel on the prediction stream plans
+ * right after it selects, into a workspace of the layer (the slot map the
+ * attention reads stays untouched), and the transfer stream only copies and
+ * commits. Moving the plan pays when the transfer stream is the longer one and
+ * its workgroups would plan several passes of pairs each (measured on MI355X:
+ * 32 layers x 64 requests +4 %; 8 x 131,072 tokens -16 %, 32 requests of
+ * 16K-32K tokens -13 %, 16 x 65,536 tokens at B = 32 -23 %). Both give the same
+ * slot maps, stamps, counts and pools. Takes effect from the next step issued.
+ * Errors: INVALID_ARG for a NULL pipeline or another value. */
+#define OASIS_PLAN_ON_TRANSFER 0
+#define OASIS_PLAN_ON_PREDICTION 1
+OASIS_API oasis_status oasis_pipeline_set_plan_stream(oasis_pipeline* pipeline, int32_t where);
 
 /* Issue one decode step of `layer` (see above). q: bf16 device [R][T][Hq][d];
  * ctx_len: device [R]; prev_ctx_len (nullable, device [R]): the lengths at the

@@ -10,5 +10,6 @@ from ._lib import (  # noqa: F401
     oasis_sparse_decode_attn, oasis_stage_blocks, OasisLayerBuffers, oasis_pipeline_create,
     oasis_pipeline_set_layer, oasis_pipeline_step, oasis_pipeline_join, oasis_pipeline_destroy,
     oasis_pipeline_profile_begin, oasis_pipeline_profile_end, oasis_update_summaries, oasis_copy_blocks,
-    oasis_union_selection,
+    oasis_union_selection, oasis_pipeline_set_local_source, oasis_pipeline_set_plan_stream, PLAN_ON_TRANSFER,
+    PLAN_ON_PREDICTION,
 )

@@ -25,7 +25,8 @@ EXPORTS = (
     "oasis_copy_blocks", "oasis_score_blocks",
     "oasis_select_topk", "oasis_stage_blocks",
     "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn", "oasis_union_selection",
-    "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_set_local_source", "oasis_pipeline_step",
+    "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_set_local_source",
+    "oasis_pipeline_set_plan_stream", "oasis_pipeline_step",
     "oasis_pipeline_join",
     "oasis_pipeline_destroy", "oasis_pipeline_profile_begin", "oasis_pipeline_profile_end",
 )
@@ -58,7 +59,7 @@ def dims(num_reqs, num_q_heads, num_kv_heads, head_dim, block_size, max_blocks) 
 
 
 _lib = None
-ABI_VERSION = 4  # OASIS_ABI_VERSION of include/oasis.h
+ABI_VERSION = 5  # OASIS_ABI_VERSION of include/oasis.h
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -109,6 +110,8 @@ def lib() -> ctypes.CDLL:
         L.oasis_pipeline_set_layer.argtypes = [_P, _I32, ctypes.POINTER(OasisLayerBuffers)]
         L.oasis_pipeline_set_local_source.restype = _I32
         L.oasis_pipeline_set_local_source.argtypes = [_P, _P, _P, _I64, _P]
+        L.oasis_pipeline_set_plan_stream.restype = _I32
+        L.oasis_pipeline_set_plan_stream.argtypes = [_P, _I32]
         L.oasis_pipeline_step.restype = _I32
         L.oasis_pipeline_step.argtypes = [_P, _I32, _P, _P, _P, _I32, _I32, _I32, _P, _P]
         L.oasis_pipeline_join.restype = _I32
@@ -339,6 +342,16 @@ def oasis_pipeline_create(d: OasisDims, num_q_tokens: int, first_draft: int, num
     _PIPE_SIZES[h.value] = (d.num_reqs * int(num_q_tokens) * d.num_q_heads * d.head_dim, d.num_reqs,
                             d.num_reqs * d.num_kv_heads)
     return h.value
+
+
+PLAN_ON_TRANSFER = 0    # OASIS_PLAN_ON_TRANSFER
+PLAN_ON_PREDICTION = 1  # OASIS_PLAN_ON_PREDICTION
+
+
+def oasis_pipeline_set_plan_stream(handle: int, where: int) -> None:
+    """Plan each step's transfer on the transfer stream (PLAN_ON_TRANSFER) or in the top-K kernel
+    on the prediction stream (PLAN_ON_PREDICTION)."""
+    _check("oasis_pipeline_set_plan_stream", lib().oasis_pipeline_set_plan_stream(handle, int(where)))
 
 
 def oasis_pipeline_set_local_source(handle: int, d: OasisDims, k_pages, v_pages, block_table) -> None:

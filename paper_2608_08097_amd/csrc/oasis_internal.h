@@ -163,7 +163,19 @@ struct StageArgs {
   int R, Hkv, B, NBmax, k, step, copy_local;
   int fetch_cap;            // admitted misses per (request, KV head), >= k: all
   int local_only;           // no selection: refresh the local block only
+  // kStagePlanCopy: plan, update slot_map / slot_stamp, copy. kStagePlanOnly:
+  // plan into `ws` (new map and stamp rows, admitted entries, their counts),
+  // leaving slot_map / slot_stamp as they are; nothing is copied. kStageCopyOnly:
+  // copy the entries in `ws` and commit its rows to slot_map / slot_stamp.
+  int mode;
+  int32_t* ws;              // stage_ws_ints(R * Hkv, k) ints (modes 1 and 2)
 };
+constexpr int kStagePlanCopy = 0, kStagePlanOnly = 1, kStageCopyOnly = 2;
+// Plan workspace: [nrh][k] map rows, [nrh][k] stamp rows, [nrh][k][2] entries (slot, page), [nrh] counts.
+inline size_t stage_ws_ints(long long nrh, int k) { return (size_t)nrh * (4 * (size_t)k + 1); }
+// Top-K (as launch_topk) and the staging plan of each (request, KV head) in one
+// kernel; a.mode must be kStagePlanOnly (the plan goes to a.ws).
+hipError_t launch_topk_plan(const TopkArgs& t, const StageArgs& a, hipStream_t s, const LaunchTiming& lt = {});
 hipError_t launch_stage(const StageArgs& a, hipStream_t s, const LaunchTiming& t = {});
 
 struct AttnArgs {

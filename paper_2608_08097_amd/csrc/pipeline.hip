@@ -46,6 +46,8 @@ struct oasis_pipeline {
   oasis_layer_buffers* layers;  // [max_layers]
   uint32_t* staged;             // [max_layers]: transfers issued per layer (its counter's last value)
   bool* is_set;                 // [max_layers]
+  int32_t** plan_ws;            // [max_layers]: device staging-plan workspace of each layer (set_layer)
+  bool plan_on_pred;            // OASIS_PLAN_ON_PREDICTION
   // optional profile: timing events around each kernel of the next prof_cap steps
   int32_t prof_cap, prof_n;
   hipEvent_t* prof_ev;          // [prof_cap][kProfKinds][2]
@@ -114,6 +116,11 @@ void release(oasis_pipeline* p) {
     if (p->pred) (void)hipStreamDestroy(p->pred);
     if (p->xfer) (void)hipStreamDestroy(p->xfer);
   }
+  if (p->plan_ws) {
+    for (int l = 0; l < p->max_layers; ++l)
+      if (p->plan_ws[l]) (void)hipFree(p->plan_ws[l]);
+  }
+  delete[] p->plan_ws;
   delete[] p->layers;
   delete[] p->staged;
   delete[] p->is_set;
@@ -188,7 +195,8 @@ oasis_status oasis_pipeline_create(const oasis_dims* dims, int32_t num_q_tokens,
   p->layers = new (std::nothrow) oasis_layer_buffers[max_layers]();
   p->staged = new (std::nothrow) uint32_t[max_layers]();
   p->is_set = new (std::nothrow) bool[max_layers]();
-  if (!p->layers || !p->staged || !p->is_set) {
+  p->plan_ws = new (std::nothrow) int32_t*[max_layers]();
+  if (!p->layers || !p->staged || !p->is_set || !p->plan_ws) {
     release(p);
     return fail(OASIS_ERR_HIP, "%s: out of host memory", fn);
   }
@@ -244,8 +252,26 @@ oasis_status oasis_pipeline_set_layer(oasis_pipeline* p, int32_t layer, const oa
   if (!b) return fail(OASIS_ERR_INVALID_ARG, "%s: buffers is NULL", fn);
   if (layer < 0 || layer >= p->max_layers)
     return fail(OASIS_ERR_INVALID_ARG, "%s: layer %d outside [0, %d)", fn, layer, p->max_layers);
+  if (!p->plan_ws[layer]) {  // the layer's staging plan, handed from the prediction to the transfer stream
+    const size_t bytes = sizeof(int32_t) * oasis::stage_ws_ints((long long)p->dims.num_reqs * p->dims.num_kv_heads, p->k);
+    const hipError_t e = hipMalloc(&p->plan_ws[layer], bytes > 0 ? bytes : sizeof(int32_t));
+    if (e != hipSuccess) {
+      p->plan_ws[layer] = nullptr;
+      return hip_status(e, fn);
+    }
+  }
   p->layers[layer] = *b;
   p->is_set[layer] = true;  // a transfer still pending for this layer is waited on at its next step
+  return ok();
+}
+
+oasis_status oasis_pipeline_set_plan_stream(oasis_pipeline* p, int32_t where) {
+  static const char* fn = "oasis_pipeline_set_plan_stream";
+  if (!p) return fail(OASIS_ERR_INVALID_ARG, "%s: pipeline is NULL", fn);
+  if (where != OASIS_PLAN_ON_TRANSFER && where != OASIS_PLAN_ON_PREDICTION)
+    return fail(OASIS_ERR_INVALID_ARG, "%s: where = %d is neither OASIS_PLAN_ON_TRANSFER nor OASIS_PLAN_ON_PREDICTION",
+                fn, where);
+  p->plan_on_pred = where == OASIS_PLAN_ON_PREDICTION;
   return ok();
 }
 
@@ -283,6 +309,16 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
                                    nullptr, &la, fn)) != OASIS_OK)
     return st;
   if (d->num_reqs == 0) return ok();
+  // OASIS_PLAN_ON_PREDICTION: the plan runs in the top-K kernel, into the
+  // layer's workspace (the slot map stays as the attention reads it); the
+  // transfer stream then only copies and commits the planned rows.
+  oasis::StageArgs gp = ga;
+  if (p->plan_on_pred) {
+    gp.mode = oasis::kStagePlanOnly;
+    gp.ws = p->plan_ws[layer];
+    ga.mode = oasis::kStageCopyOnly;
+    ga.ws = p->plan_ws[layer];
+  }
   // compressed keys of the blocks completed since prev_ctx_len, read from the
   // local-block source (where the newest tokens are), before the scoring
   const oasis::SummaryArgs ua{p->local_k, p->local_num_pages, p->local_block_table, ctx_len, b.kmax, b.kmin,
@@ -306,7 +342,10 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   HIP_TRY(signal(p, fg, kAttn, ++cnt[kAttn]), fn);
   if (prev_ctx_len) HIP_TRY(oasis::launch_summaries(ua, p->pred), fn);
   HIP_TRY(oasis::launch_score(sa, p->pred, prof_timing(p, 1)), fn);
-  HIP_TRY(oasis::launch_topk(ta, p->pred, prof_timing(p, 2)), fn);
+  if (p->plan_on_pred)
+    HIP_TRY(oasis::launch_topk_plan(ta, gp, p->pred, prof_timing(p, 2)), fn);
+  else
+    HIP_TRY(oasis::launch_topk(ta, p->pred, prof_timing(p, 2)), fn);
   HIP_TRY(signal(p, p->pred, kPred, ++cnt[kPred]), fn);
   HIP_TRY(wait_for(p, p->xfer, kPred, cnt[kPred]), fn);
   HIP_TRY(wait_for(p, p->xfer, kAttn, cnt[kAttn]), fn);  // the gather overwrites slots the attention reads

@@ -76,12 +76,17 @@ __device__ int select_exclusive_scan(int v, int* s_wave) {
 }
 
 // Select the top k of s[0..n) into out[0..k) (ascending ids, -1 padded when
-// n < k) and set *count; every thread of the workgroup calls it.
+// n < k) and set *count; every thread of the workgroup calls it. With lout
+// (LDS, k entries) the selection is also left there for the workgroup.
 template <int NTHR, int KPT>
-__device__ void select_row(const float* s, int n, int k, int32_t* out, int32_t* count, SelectShared<NTHR, KPT>& sh) {
+__device__ void select_row(const float* s, int n, int k, int32_t* out, int32_t* count, SelectShared<NTHR, KPT>& sh,
+                           int* lout = nullptr) {
   const int tid = threadIdx.x;
   if (n <= k) {  // every candidate fits the budget
-    for (int i = tid; i < k; i += NTHR) out[i] = i < n ? i : -1;
+    for (int i = tid; i < k; i += NTHR) {
+      out[i] = i < n ? i : -1;
+      if (lout) lout[i] = i < n ? i : -1;
+    }
     if (tid == 0) *count = n;
     return;
   }
@@ -233,7 +238,11 @@ __device__ void select_row(const float* s, int n, int k, int32_t* out, int32_t* 
       take = all_eq || eq_rank < need_eq;
       ++eq_rank;
     }
-    if (take && pos < k) out[pos++] = lo + j;
+    if (take && pos < k) {
+      out[pos] = lo + j;
+      if (lout) lout[pos] = lo + j;
+      ++pos;
+    }
   }
   if (tid == 0) *count = k;
 }

@@ -50,6 +50,7 @@
 #include <climits>
 
 #include "oasis_internal.h"
+#include "select.h"
 
 namespace oasis {
 
@@ -57,7 +58,7 @@ namespace {
 
 constexpr int kPlanThreads = 256;
 constexpr int kMaxK = 1024;
-constexpr int kPer = kMaxK / kPlanThreads;  // items per thread in the scans
+constexpr int kPer = kMaxK / kPlanThreads;  // items per thread of the staging kernel's passes
 constexpr int kMaxPairs = 64;  // (request, KV head) pairs planned in one pass, at most
 constexpr int kCopyWorkgroups = 32;
 constexpr int kCopyInflightMin = 64;  // block-head entries (K and V) in flight over the whole grid, at least
@@ -70,7 +71,11 @@ __device__ inline unsigned order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Exclusive scan over an NTHR-thread workgroup; the total is left in
+// s_wave[NTHR / 64] (s_wave holds NTHR / 64 + 1 ints).
+template <int NTHR>
 __device__ int wg_exclusive_scan(int v, int* s_wave) {
+  constexpr int kWaves = NTHR / 64;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int x = wave_incl_sum(v);
@@ -79,9 +84,9 @@ __device__ int wg_exclusive_scan(int v, int* s_wave) {
   int base = 0;
   for (int w = 0; w < wave; ++w) base += s_wave[w];
   int total = 0;
-  for (int w = 0; w < kPlanThreads / 64; ++w) total += s_wave[w];
+  for (int w = 0; w < kWaves; ++w) total += s_wave[w];
   __syncthreads();
-  if (threadIdx.x == 0) s_wave[4] = total;
+  if (threadIdx.x == 0) s_wave[kWaves] = total;
   __syncthreads();
   return base + x - v;
 }
@@ -98,8 +103,15 @@ __device__ int wg_exclusive_scan(int v, int* s_wave) {
 // compacted item against the others of its pair (misses by score under a cap,
 // stale slots by (stamp, slot)). Planning the pairs of a workgroup in one pass
 // pays the dependent global reads and the barriers once, not once per pair.
+//
+// With lsel (one pair, np = 1) the selection is taken from LDS (lsel[0, lsel_m)
+// ascending) instead of a.sel / a.sel_count. NTHR threads call it (256 in the
+// staging kernel, 1024 in the fused top-K and plan kernel).
+template <int NTHR>
 __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int* s_slot, int* s_page, int* s_epair,
-                         int* s_prh, int* s_wave) {
+                         int* s_prh, int* s_wave, const int* lsel = nullptr, int lsel_m = 0) {
+  constexpr int kPer = kMaxK / NTHR;  // items per thread in the scans
+  constexpr int kTot = NTHR / 64;     // where wg_exclusive_scan leaves its total
   const int tid = threadIdx.x;
   const int k = a.k;
   const int N = np * k;
@@ -111,7 +123,7 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
   __shared__ int s_midx[kMaxK], s_madm[kMaxK], s_skey[kMaxK], s_sslot[kMaxK], s_vstale[kMaxK], s_free[kMaxK];
   // per pair: selected count, run starts of misses / free / stale items (np + 1 entries), admitted start, moved
   __shared__ int s_pm[kMaxPairs], s_mstart[kMaxPairs + 1], s_fstart[kMaxPairs + 1], s_sstart[kMaxPairs + 1];
-  __shared__ int s_astart[kMaxPairs], s_moved[kMaxPairs];
+  __shared__ int s_astart[kMaxPairs], s_moved[kMaxPairs], s_nadm[kMaxPairs];
 
   // The page of every selected block (and, when a cap may bind, its score) is
   // fetched as soon as the block id arrives, so that these dependent loads
@@ -120,7 +132,7 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
   unsigned ky[kPer];
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
-    const int i = tid + j * kPlanThreads;
+    const int i = tid + j * NTHR;
     pg[j] = -1;
     ky[j] = 0u;
     if (i < N) {
@@ -128,8 +140,8 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
       const int li = i - p * k;
       const int rh = pair0 + p * stride;
       const long long row = (long long)rh * k;
-      const int sv = a.sel[row + li];  // in the row (k entries); loaded without waiting for the count
-      int m = a.sel_count[rh];
+      const int sv = lsel ? lsel[li] : a.sel[row + li];  // in the row (k entries); loaded without waiting for the count
+      int m = lsel ? lsel_m : a.sel_count[rh];
       m = m < 0 ? 0 : (m > k ? k : m);
       const int b = li < m ? sv : INT_MAX;
       s_sel[i] = b;
@@ -140,6 +152,7 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
         s_pm[p] = m;
         s_prh[p] = rh;
         s_moved[p] = 0;
+        s_nadm[p] = 0;
       }
       if (li < m) {
         const int r = rh / a.Hkv;
@@ -152,7 +165,7 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
   __syncthreads();
 
   // resident hits: binary search of every resident block in its pair's (ascending) selection
-  for (int s = tid; s < N; s += kPlanThreads) {
+  for (int s = tid; s < N; s += NTHR) {
     const int p = s / k;
     const int off = p * k;
     const int m = s_pm[p];
@@ -173,7 +186,7 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
   }
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
-    const int i = tid + j * kPlanThreads;
+    const int i = tid + j * NTHR;
     if (i < N) {
       s_selpage[i] = pg[j];
       s_selkey[i] = ky[j];
@@ -194,10 +207,10 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
       else if (!s_keep[i]) ++ns;
     }
   }
-  const int mf_base = wg_exclusive_scan(nm | (nf << 16), s_wave);  // two 16-bit counts (<= 1024 each)
-  const int mf_tot = s_wave[4];
-  const int st_base = wg_exclusive_scan(ns, s_wave);
-  const int n_stale = s_wave[4];
+  const int mf_base = wg_exclusive_scan<NTHR>(nm | (nf << 16), s_wave);  // two 16-bit counts (<= 1024 each)
+  const int mf_tot = s_wave[kTot];
+  const int st_base = wg_exclusive_scan<NTHR>(ns, s_wave);
+  const int n_stale = s_wave[kTot];
   const int n_miss = mf_tot & 0xFFFF;
   const int n_free = mf_tot >> 16;
   {
@@ -239,7 +252,7 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
   // with the highest score (ties: lowest block id). Keys are order-preserving
   // integers, so the ranks are distinct even for NaN scores and exactly
   // fetch_cap misses are admitted.
-  for (int c = tid; c < n_miss; c += kPlanThreads) {
+  for (int c = tid; c < n_miss; c += NTHR) {
     const int p = s_midx[c] / k;
     const int ms = s_mstart[p], me = s_mstart[p + 1];
     int adm = 1;
@@ -256,7 +269,7 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
     s_madm[c] = adm;
   }
   // victim order per pair: free slots ascending (s_free), then stale slots by (stamp, slot)
-  for (int c = tid; c < n_stale; c += kPlanThreads) {
+  for (int c = tid; c < n_stale; c += NTHR) {
     const int p = s_sslot[c] / k;
     const int ss = s_sstart[p], se = s_sstart[p + 1];
     const int st = s_skey[c];
@@ -277,8 +290,8 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
     const int c = i0 + j;
     if (c < n_miss && s_madm[c]) ++na;
   }
-  const int adm_base = wg_exclusive_scan(na, s_wave);
-  const int n_adm = s_wave[4];
+  const int adm_base = wg_exclusive_scan<NTHR>(na, s_wave);
+  const int n_adm = s_wave[kTot];
   {
     int ar = adm_base;
 #pragma unroll
@@ -316,20 +329,112 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
         s_keep[v] = page >= 0;
       }
       if (page >= 0) atomicAdd(&s_moved[p], 1);
+      atomicAdd(&s_nadm[p], 1);
       ++ar;
     }
   }
   __syncthreads();
 
-  for (int s = tid; s < N; s += kPlanThreads) {
-    const int p = s / k;
-    const long long at = (long long)s_prh[p] * k + (s - p * k);
-    a.slot_map[at] = s_map[s];
-    if (s_keep[s]) a.slot_stamp[at] = a.step;
+  if (a.mode == kStagePlanOnly) {
+    // the new rows, the admitted entries and their counts go to the workspace
+    const long long nrhk = (long long)a.R * a.Hkv * k;
+    int32_t* ws_map = a.ws;
+    int32_t* ws_stamp = a.ws + nrhk;
+    int2* ws_ent = reinterpret_cast<int2*>(a.ws + 2 * nrhk);
+    int32_t* ws_cnt = a.ws + 4 * nrhk;
+    for (int s = tid; s < N; s += NTHR) {
+      const int p = s / k;
+      const long long at = (long long)s_prh[p] * k + (s - p * k);
+      ws_map[at] = s_map[s];
+      ws_stamp[at] = s_keep[s] ? a.step : s_stamp[s];
+    }
+    for (int e = tid; e < n_adm; e += NTHR) {
+      const int p = s_epair[e];
+      ws_ent[(long long)s_prh[p] * k + (e - s_astart[p])] = make_int2(s_slot[e], s_page[e]);
+    }
+    for (int p = tid; p < np; p += NTHR) ws_cnt[s_prh[p]] = s_nadm[p];
+  } else {
+    for (int s = tid; s < N; s += NTHR) {
+      const int p = s / k;
+      const long long at = (long long)s_prh[p] * k + (s - p * k);
+      a.slot_map[at] = s_map[s];
+      if (s_keep[s]) a.slot_stamp[at] = a.step;
+    }
   }
   if (a.moved)
-    for (int p = tid; p < np; p += kPlanThreads) a.moved[s_prh[p]] = s_moved[p];
+    for (int p = tid; p < np; p += NTHR) a.moved[s_prh[p]] = s_moved[p];
   return n_adm;
+}
+
+// Entries of a pass planned earlier (kStagePlanOnly): per pair its admitted
+// (slot, page) entries from the workspace, compacted over the pass's pairs in
+// LDS; the counts and all k entries of every pair are loaded together.
+__device__ int load_planned(const StageArgs& a, int pair0, int np, int stride, int* s_slot, int* s_page,
+                            int* s_epair, int* s_prh) {
+  const int tid = threadIdx.x;
+  const int k = a.k;
+  const int N = np * k;
+  const long long nrhk = (long long)a.R * a.Hkv * k;
+  const int2* ws_ent = reinterpret_cast<const int2*>(a.ws + 2 * nrhk);
+  const int32_t* ws_cnt = a.ws + 4 * nrhk;
+  __shared__ int s_cnt[kMaxPairs], s_off[kMaxPairs + 1];
+  int2 ent[kPer];
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int i = tid + j * kPlanThreads;
+    ent[j] = make_int2(-1, -1);
+    if (i < N) {
+      const int p = i / k;
+      ent[j] = ws_ent[(long long)(pair0 + p * stride) * k + (i - p * k)];
+    }
+  }
+  for (int p = tid; p < np; p += kPlanThreads) {
+    const int rh = pair0 + p * stride;
+    const int c = ws_cnt[rh];
+    s_cnt[p] = c < 0 ? 0 : (c > k ? k : c);
+    s_prh[p] = rh;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int o = 0;
+    for (int p = 0; p < np; ++p) {
+      s_off[p] = o;
+      o += s_cnt[p];
+    }
+    s_off[np] = o;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kPer; ++j) {
+    const int i = tid + j * kPlanThreads;
+    if (i < N) {
+      const int p = i / k;
+      const int li = i - p * k;
+      if (li < s_cnt[p]) {
+        const int e = s_off[p] + li;
+        int page = ent[j].y;
+        if (page < 0 || page >= a.num_pages) page = -1;
+        s_slot[e] = ent[j].x;
+        s_page[e] = page;
+        s_epair[e] = p;
+      }
+    }
+  }
+  return s_off[np];
+}
+
+// Commit the workspace rows of a pass's pairs to slot_map / slot_stamp.
+__device__ void commit_planned(const StageArgs& a, int np, const int* s_prh) {
+  const int k = a.k;
+  const long long nrhk = (long long)a.R * a.Hkv * k;
+  const int32_t* ws_map = a.ws;
+  const int32_t* ws_stamp = a.ws + nrhk;
+  for (int s = threadIdx.x; s < np * k; s += kPlanThreads) {
+    const int p = s / k;
+    const long long at = (long long)s_prh[p] * k + (s - p * k);
+    a.slot_map[at] = ws_map[at];
+    a.slot_stamp[at] = ws_stamp[at];
+  }
 }
 
 // One batch of PF block-head entries held in registers (K and V, 16-byte
@@ -452,8 +557,10 @@ __global__ __launch_bounds__(kPlanThreads) void stage_kernel(StageArgs a) {
     int n = 0;
     if (a.local_only) {
       for (int p = tid; p < np; p += kPlanThreads) s_prh[p] = pair0 + p * stride;
+    } else if (a.mode == kStageCopyOnly) {
+      n = load_planned(a, pair0, np, stride, s_slot, s_page, s_epair, s_prh);
     } else {
-      n = plan_pass(a, pair0, np, stride, s_slot, s_page, s_epair, s_prh, s_wave);
+      n = plan_pass<kPlanThreads>(a, pair0, np, stride, s_slot, s_page, s_epair, s_prh, s_wave);
     }
     if (a.copy_local) {  // the local block of every pair of the pass, into slot k
       for (int p = tid; p < np; p += kPlanThreads) {
@@ -476,8 +583,33 @@ __global__ __launch_bounds__(kPlanThreads) void stage_kernel(StageArgs a) {
     // entry past the end (or without a page) reads the start of the pool
     // instead (device memory, discarded), so the wait counts stay exact.
     copy_entries<BS, PF>(a, n, s_slot, s_page, s_epair, s_prh, tile);
+    if (a.mode == kStageCopyOnly && !a.local_only) commit_planned(a, np, s_prh);
     __syncthreads();  // LDS plan arrays are reused by the next pass
   }
+}
+
+// Top-K and plan in one kernel (the layer pipeline's prediction stream): a
+// 1024-thread workgroup per (request, KV head) selects as the top-K kernel
+// does, keeps the selection in LDS and plans the pair's transfer from it into
+// the workspace (kStagePlanOnly), so the plan costs neither a launch nor a
+// re-read of the selection, and the transfer stream only copies.
+constexpr int kSelThreads = 1024;
+
+template <int KPT>
+__global__ __launch_bounds__(kSelThreads) void topk_plan_kernel(TopkArgs t, StageArgs a) {
+  __shared__ SelectShared<kSelThreads, KPT> sh;
+  __shared__ int s_lsel[kMaxK];
+  __shared__ int s_slot[kMaxK + kMaxPairs], s_page[kMaxK + kMaxPairs], s_epair[kMaxK + kMaxPairs];
+  __shared__ int s_prh[kMaxPairs];
+  __shared__ int s_wave[kSelThreads / 64 + 1];
+  const int rh = blockIdx.x;
+  const int r = rh / t.Hkv;
+  const Ctx c = ctx_blocks(t.ctx_len[r], t.B, t.NBmax);
+  select_row<kSelThreads, KPT>(t.scores + (long long)rh * t.NBmax, c.n_cand, t.k, t.sel + (long long)rh * t.k,
+                               t.sel_count + rh, sh, s_lsel);
+  __syncthreads();
+  const int m = c.n_cand < t.k ? (c.n_cand > 0 ? c.n_cand : 0) : t.k;
+  plan_pass<kSelThreads>(a, rh, 1, 1, s_slot, s_page, s_epair, s_prh, s_wave, s_lsel, m);
 }
 
 }  // namespace
@@ -503,6 +635,22 @@ hipError_t launch_bs(const StageArgs& a, hipStream_t s, const LaunchTiming& t) {
     launch_kernel(stage_kernel<BS, 2>, dim3(grid), dim3(kPlanThreads), s, t, a);
   else
     launch_kernel(stage_kernel<BS, 1>, dim3(grid), dim3(kPlanThreads), s, t, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_plan(const TopkArgs& t, const StageArgs& a, hipStream_t s, const LaunchTiming& lt) {
+  if (a.mode != kStagePlanOnly || !a.ws || a.local_only) return hipErrorInvalidValue;
+  // the candidate count of every request is at most NBmax - 1; beyond 16 keys
+  // per thread they are re-read from memory (the staged row would not fit LDS
+  // next to the plan)
+  const int per = (t.NBmax + kSelThreads - 1) / kSelThreads;
+  const dim3 grid((unsigned)(t.R * t.Hkv));
+  if (per <= 8)
+    launch_kernel(topk_plan_kernel<8>, grid, dim3(kSelThreads), s, lt, t, a);
+  else if (per <= 16)
+    launch_kernel(topk_plan_kernel<16>, grid, dim3(kSelThreads), s, lt, t, a);
+  else
+    launch_kernel(topk_plan_kernel<0>, grid, dim3(kSelThreads), s, lt, t, a);
   return hipGetLastError();
 }
 

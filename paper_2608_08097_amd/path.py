@@ -91,8 +91,11 @@ class DecodePath:
     def __init__(self, d: L.OasisDims, num_q_tokens: int, k: int, host_k: torch.Tensor, host_v: torch.Tensor,
                  block_table: torch.Tensor, first_draft: int = 1, num_draft: int | None = None,
                  scale: float | None = None, fetch_cap: int | None = None, native: bool = True,
-                 max_layers: int = 256, streams: tuple | None = None):
+                 max_layers: int = 256, streams: tuple | None = None, plan_on_prediction: bool = False):
         self.dims, self.T, self.k = d, int(num_q_tokens), int(k)
+        # native issuer: plan each step's transfer in the top-K kernel on the
+        # prediction stream instead of in the staging kernel on the transfer stream
+        self.plan_on_prediction = bool(plan_on_prediction)
         # step_pipelined issues through the library's native step issuer unless a timer is given
         self.native = bool(native)
         self.max_layers = int(max_layers)
@@ -122,6 +125,8 @@ class DecodePath:
                                                  self.block_table, self.max_layers, self.side, self.xfer)
             if self.local_source is not None:
                 L.oasis_pipeline_set_local_source(self._pipe, self.dims, *self.local_source)
+            if self.plan_on_prediction:
+                L.oasis_pipeline_set_plan_stream(self._pipe, L.PLAN_ON_PREDICTION)
         lid = getattr(st, "layer_id", None)
         if lid is None or getattr(st, "pipe", None) != self._pipe:
             if self._n_layers >= self.max_layers:

@@ -48,7 +48,7 @@ def test_exports_match_header(lib):
 
 
 def test_abi_version(lib):
-    assert lib.oasis_abi_version() == 4
+    assert lib.oasis_abi_version() == 5
 
 
 def test_argument_checks_without_gpu(lib):
@@ -119,6 +119,7 @@ def test_pipeline_argument_checks_without_gpu(lib):
     assert L.oasis_pipeline_profile_begin(None, 4) == 1
     assert L.oasis_pipeline_profile_end(None, None, None, None) == 1
     assert L.oasis_pipeline_set_local_source(None, None, None, 0, None) == 1
+    assert L.oasis_pipeline_set_plan_stream(None, 0) == 1
     L.oasis_pipeline_destroy(None)
 
 

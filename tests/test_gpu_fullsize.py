@@ -133,9 +133,11 @@ def test_fullsize_pipelined_capped_c4():
     path.close()
 
 
-def test_fullsize_growing_c3():
+@pytest.mark.parametrize("plan_pred", [False, True])
+def test_fullsize_growing_c3(plan_pred):
     """The reasoning loop: 64 requests (1K prompt + 4K-16K generated), one token per step, summary
-    updates on block completion, two layer states; a sampled request against its oracle chain."""
+    updates on block completion, two layer states; a sampled request against its oracle chain. The
+    benchmark plans this loop's transfers on the prediction stream (``plan_pred``)."""
     NL, S, cap = 2, 20, 6
     w, hk_t, hv_t = _tier("c3", steps=S)
     c = w.cfg
@@ -145,11 +147,11 @@ def test_fullsize_growing_c3():
     ctx_dev = [dev_i32(w.ctx_len(s)) for s in range(S)]
     qs = [w.layer_queries(l, S) for l in range(NL)]
     q_dev = [[dev_bf16(x) for x in qs[l]] for l in range(NL)]
-    path = DecodePath(d, c.T, K, hk_t, hv_t, bt, fetch_cap=cap)
+    path = DecodePath(d, c.T, K, hk_t, hv_t, bt, fetch_cap=cap, plan_on_prediction=plan_pred)
     layers = [path.new_layer() for _ in range(NL)]
     for st in layers:
         path.build_summaries(st, ctx_dev[0])
-    note("full-size growing c3: issuing")
+    note(f"full-size growing c3 (plan on prediction: {plan_pred}): issuing")
     for s in range(S):
         for l, st in enumerate(layers):
             if s:

@@ -455,13 +455,14 @@ def test_dense_equivalence():
     assert_lse_close(st.lse.cpu().numpy(), ref_l)
 
 
-@pytest.mark.parametrize("issue", ["native", "python"])
+@pytest.mark.parametrize("issue", ["native", "native_plan_pred", "python"])
 @pytest.mark.parametrize("cap", [None, 2])
 def test_pipelined_multistep(cap, issue):
     """Reasoning-style loop: AR(1) queries, one token per step, attention on the previous step's staging.
 
     With a fetch cap, later steps attend stale residents in place of the misses
-    that were not admitted (paper §5.5.1), on both sides alike.
+    that were not admitted (paper §5.5.1), on both sides alike. ``native_plan_pred``
+    plans each transfer in the top-K kernel on the prediction stream.
     """
     steps = 6
     w = make_workload("c3", num_reqs=3, ctx_args=(200, 300, 1400), steps=steps, budget=16 * 24)
@@ -470,7 +471,8 @@ def test_pipelined_multistep(cap, issue):
     hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
     d = _dims(w)
     k = c.K
-    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap, native=issue == "native")
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap, native=issue != "python",
+                      plan_on_prediction=issue == "native_plan_pred")
     st = LayerState(d, c.T, k)
     smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
     stamp = np.zeros_like(smap)
@@ -507,10 +509,12 @@ def test_pipelined_multistep(cap, issue):
             assert moved.max() <= cap
 
 
-def test_pipelined_layers_native():
+@pytest.mark.parametrize("plan_pred", [False, True])
+def test_pipelined_layers_native(plan_pred):
     """Several layers interleaved on the native issuer with no host synchronization
     between steps (paper §4.2.2: per-layer chains, layer-local waits); every
-    layer's final state equals its own oracle chain."""
+    layer's final state equals its own oracle chain, with the transfer planned on
+    either stream."""
     n_layers, rounds, cap = 3, 4, 3
     w = make_workload("c2", num_reqs=3, ctx_args=(900, 2500), budget=16 * 20, ar_queries=True)
     c = w.cfg
@@ -522,7 +526,7 @@ def test_pipelined_layers_native():
     ctx_d = dev_i32(ctx)
     qs = [w.layer_queries(l, rounds + 1) for l in range(n_layers)]
     kmax, kmin = O.block_summaries(hk, w.block_table, ctx, c.block_size, w.NBmax)
-    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap)
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap, plan_on_prediction=plan_pred)
     layers = [LayerState(d, c.T, k) for _ in range(n_layers)]
     ref = []
     for l, st in enumerate(layers):
@@ -539,7 +543,7 @@ def test_pipelined_layers_native():
         O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, 0, pk, pv, ctx, c.block_size)
         ref.append(dict(smap=smap, stamp=stamp, pk=pk, pv=pv))
     q_dev = [[dev_bf16(x) for x in qs[l]] for l in range(n_layers)]
-    note("native pipelined layers: issuing")
+    note(f"native pipelined layers: issuing (plan on prediction: {plan_pred})")
     for s in range(1, rounds + 1):
         for l in range(n_layers):
             path.step_pipelined(layers[l], q_dev[l][s], ctx_d, s)
@@ -622,6 +626,9 @@ def test_pipeline_abi_errors_on_device():
         assert e.value.status == 1 and "max_new_blocks" in str(e.value)
         # a local-block source needs all three of k_pages, v_pages and block_table
         assert P._lib.lib().oasis_pipeline_set_local_source(h, hk_t.data_ptr(), None, 1, None) == 1
+        with pytest.raises(P.OasisError) as e:  # neither plan stream
+            P.oasis_pipeline_set_plan_stream(h, 2)
+        assert e.value.status == 1 and "where" in str(e.value)
         with pytest.raises(P.OasisError) as e:
             P.oasis_pipeline_set_layer(h, 4, d, c.T, c.K, st.kmax, st.kmin, st.scores, st.sel, st.sel_count,
                                        st.slot_map, st.slot_stamp, st.pool_k, st.pool_v, st.moved, st.out,

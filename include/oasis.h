@@ -303,8 +303,10 @@ OASIS_API oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const ui
  * them. Ownership: every pointer stays the caller's and must outlive the
  * pipeline's use of it (tensors read by a step stay alive until the layer's
  * next step or a join); the pipeline owns its counter array (hipMalloc at
- * create, 256 bytes per counter, (5 + max_layers) counters) and the two
- * background streams when it creates them. host_k/host_v are resolved to
+ * create, 256 bytes per counter, (5 + max_layers) counters), one staging-plan
+ * workspace per registered layer (hipMalloc at the layer's first set_layer,
+ * R * Hkv * (4 * k + 1) int32) and the two background streams when it creates
+ * them; destroy frees them. host_k/host_v are resolved to
  * device-visible addresses once, at create. All calls for one pipeline must come
  * from one host thread with the creating device current.
  */
@@ -338,7 +340,9 @@ OASIS_API oasis_status oasis_pipeline_create(const oasis_dims* dims, int32_t num
                                    void* xfer_stream, oasis_pipeline** pipeline);
 
 /* Register (or replace) the buffers of layer `layer` (0 <= layer < max_layers). A
- * transfer already issued for the layer is still waited on at its next step. */
+ * transfer already issued for the layer is still waited on at its next step.
+ * Errors: INVALID_ARG for a NULL pipeline or buffers or a layer out of range;
+ * HIP when the layer's plan workspace cannot be allocated. */
 OASIS_API oasis_status oasis_pipeline_set_layer(oasis_pipeline* pipeline, int32_t layer,
                                       const oasis_layer_buffers* buffers);
 

@@ -568,6 +568,63 @@ def test_pipelined_layers_native(plan_pred):
     path.close()
 
 
+@pytest.mark.parametrize("plan_pred", [False, True])
+def test_pipelined_large_k_b32(plan_pred):
+    """The pipelined step at block size 32 with k = 1,024 (one (request, KV head) pair per plan pass,
+    72 query rows per KV head) and a binding fetch cap, the transfer planned on either stream;
+    slot maps, stamps, pools and the last attention equal the oracle chain."""
+    rounds, cap = 3, 48
+    w = make_workload("c5", num_reqs=2, ctx_args=(40000,), budget=32 * 1024, ar_queries=True)
+    c = w.cfg
+    k = c.K
+    hk_t, hv_t = pinned_pages(w)
+    hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
+    d = _dims(w)
+    ctx = w.ctx_len(0)
+    ctx_d = dev_i32(ctx)
+    qs = w.layer_queries(0, rounds + 1)
+    kmax, kmin = O.block_summaries(hk, w.block_table, ctx, c.block_size, w.NBmax)
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap, plan_on_prediction=plan_pred)
+    st = LayerState(d, c.T, k)
+    path.build_summaries(st, ctx_d)
+    path.predict(st, dev_bf16(qs[0]), ctx_d)
+    path.stage(st, ctx_d, 0, fetch_cap=k)
+    smap = np.full((c.num_reqs, c.num_kv_heads, k), -1, np.int32)
+    stamp = np.zeros_like(smap)
+    pk = np.zeros((c.num_reqs, k + 1, c.num_kv_heads, c.block_size, c.head_dim), np.uint16)
+    pv = np.zeros_like(pk)
+    sc = O.block_scores(qs[0], kmax, kmin, ctx, c.num_kv_heads, c.block_size)
+    sel, cnt = O.select_topk(sc, ctx, k, c.block_size)
+    O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, 0, pk, pv, ctx, c.block_size)
+    q_dev = [dev_bf16(x) for x in qs]
+    note(f"pipelined k=1024 B=32 (plan on prediction: {plan_pred}): issuing")
+    for s in range(1, rounds + 1):
+        path.step_pipelined(st, q_dev[s], ctx_d, s)
+    path.join()
+    torch.cuda.synchronize()
+    moved_total = 0
+    for s in range(1, rounds + 1):
+        q = qs[s]
+        if s == rounds:
+            ref_o, ref_l = O.sparse_attend(q, pk, pv, smap, ctx, c.block_size)
+        sc = O.block_scores(q, kmax, kmin, ctx, c.num_kv_heads, c.block_size)
+        sel, cnt = O.select_topk(sc, ctx, k, c.block_size)
+        moved = O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, s, pk, pv, ctx, c.block_size,
+                               copy_local=False, scores=sc, fetch_cap=cap)
+        assert moved.max() <= cap
+        moved_total += int(moved.sum())
+    assert moved_total > 0
+    assert_attn_close(host_bits(st.out), ref_o, "k=1024 out")
+    assert_lse_close(st.lse.cpu().numpy(), ref_l)
+    assert not selection_diff(st.sel.cpu().numpy(), st.sel_count.cpu().numpy(), sel, cnt, sc)
+    assert np.array_equal(st.moved.cpu().numpy(), moved)
+    assert np.array_equal(st.slot_map.cpu().numpy(), smap)
+    assert np.array_equal(st.slot_stamp.cpu().numpy(), stamp)
+    assert np.array_equal(host_bits(st.pool_k), pk)
+    assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), pv)
+    path.close()
+
+
 def test_pipeline_profile():
     """The native issuer's kernel timing records one span per kernel kind per step."""
     w = make_workload("c2", num_reqs=2, ctx_args=(3000, 5000), budget=16 * 32, ar_queries=True)

@@ -248,8 +248,9 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build measures one GPU only; --gpus N with N > 1 is not supported "
-              "(the path has no cross-GPU step; see the sharding notes in DESIGN.md)", file=sys.stderr)
+        print("bench.py: measures one GPU only; --gpus N with N > 1 is not supported (the path has no "
+              "cross-GPU step: requests and KV heads would be split over GPUs, each running this path alone)",
+              file=sys.stderr)
         sys.exit(2)
     if args.copy_calib:
         copy_calibration()

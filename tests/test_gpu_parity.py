@@ -697,7 +697,7 @@ def test_pipeline_abi_errors_on_device():
 
 
 # ---------------------------------------------------------------------------
-# host-side errors through the C ABI on a GPU machine
+# host-side errors through the C ABI with a GPU present
 # ---------------------------------------------------------------------------
 
 def test_abi_errors_on_device():

@@ -303,10 +303,10 @@ OASIS_API oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const ui
  * them. Ownership: every pointer stays the caller's and must outlive the
  * pipeline's use of it (tensors read by a step stay alive until the layer's
  * next step or a join); the pipeline owns its counter array (hipMalloc at
- * create, 256 bytes per counter, (5 + max_layers) counters), one staging-plan
- * workspace per registered layer (hipMalloc at the layer's first set_layer,
- * R * Hkv * (4 * k + 1) int32) and the two background streams when it creates
- * them; destroy frees them. host_k/host_v are resolved to
+ * create, 256 bytes per counter, (5 + max_layers) counters), with the plan on
+ * the prediction stream one staging-plan workspace per registered layer
+ * (hipMalloc at set_plan_stream or set_layer, R * Hkv * (4 * k + 1) int32),
+ * and the two background streams when it creates them; destroy frees them. host_k/host_v are resolved to
  * device-visible addresses once, at create. All calls for one pipeline must come
  * from one host thread with the creating device current.
  */
@@ -342,7 +342,8 @@ OASIS_API oasis_status oasis_pipeline_create(const oasis_dims* dims, int32_t num
 /* Register (or replace) the buffers of layer `layer` (0 <= layer < max_layers). A
  * transfer already issued for the layer is still waited on at its next step.
  * Errors: INVALID_ARG for a NULL pipeline or buffers or a layer out of range;
- * HIP when the layer's plan workspace cannot be allocated. */
+ * HIP when the layer's plan workspace (OASIS_PLAN_ON_PREDICTION) cannot be
+ * allocated. */
 OASIS_API oasis_status oasis_pipeline_set_layer(oasis_pipeline* pipeline, int32_t layer,
                                       const oasis_layer_buffers* buffers);
 
@@ -369,8 +370,10 @@ OASIS_API oasis_status oasis_pipeline_set_local_source(oasis_pipeline* pipeline,
  * its workgroups would plan several passes of pairs each (measured on MI355X:
  * 32 layers x 64 requests +4 %; 8 x 131,072 tokens -16 %, 32 requests of
  * 16K-32K tokens -13 %, 16 x 65,536 tokens at B = 32 -23 %). Both give the same
- * slot maps, stamps, counts and pools. Takes effect from the next step issued.
- * Errors: INVALID_ARG for a NULL pipeline or another value. */
+ * slot maps, stamps, counts and pools. Takes effect from the next step issued;
+ * OASIS_PLAN_ON_PREDICTION allocates the plan workspace of every registered
+ * layer that has none. Errors: INVALID_ARG for a NULL pipeline or another
+ * value; HIP when a workspace cannot be allocated (the setting is unchanged). */
 #define OASIS_PLAN_ON_TRANSFER 0
 #define OASIS_PLAN_ON_PREDICTION 1
 OASIS_API oasis_status oasis_pipeline_set_plan_stream(oasis_pipeline* pipeline, int32_t where);

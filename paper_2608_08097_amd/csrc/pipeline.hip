@@ -127,6 +127,17 @@ void release(oasis_pipeline* p) {
   delete p;
 }
 
+// The staging-plan workspace of a layer (OASIS_PLAN_ON_PREDICTION hands each
+// step's plan from the prediction to the transfer stream through it); made
+// once per layer, kept until destroy.
+hipError_t alloc_plan_ws(oasis_pipeline* p, int layer) {
+  if (p->plan_ws[layer]) return hipSuccess;
+  const size_t bytes = sizeof(int32_t) * oasis::stage_ws_ints((long long)p->dims.num_reqs * p->dims.num_kv_heads, p->k);
+  const hipError_t e = hipMalloc(&p->plan_ws[layer], bytes > 0 ? bytes : sizeof(int32_t));
+  if (e != hipSuccess) p->plan_ws[layer] = nullptr;
+  return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -252,13 +263,9 @@ oasis_status oasis_pipeline_set_layer(oasis_pipeline* p, int32_t layer, const oa
   if (!b) return fail(OASIS_ERR_INVALID_ARG, "%s: buffers is NULL", fn);
   if (layer < 0 || layer >= p->max_layers)
     return fail(OASIS_ERR_INVALID_ARG, "%s: layer %d outside [0, %d)", fn, layer, p->max_layers);
-  if (!p->plan_ws[layer]) {  // the layer's staging plan, handed from the prediction to the transfer stream
-    const size_t bytes = sizeof(int32_t) * oasis::stage_ws_ints((long long)p->dims.num_reqs * p->dims.num_kv_heads, p->k);
-    const hipError_t e = hipMalloc(&p->plan_ws[layer], bytes > 0 ? bytes : sizeof(int32_t));
-    if (e != hipSuccess) {
-      p->plan_ws[layer] = nullptr;
-      return hip_status(e, fn);
-    }
+  if (p->plan_on_pred) {
+    const hipError_t e = alloc_plan_ws(p, layer);
+    if (e != hipSuccess) return hip_status(e, fn);
   }
   p->layers[layer] = *b;
   p->is_set[layer] = true;  // a transfer still pending for this layer is waited on at its next step
@@ -271,6 +278,13 @@ oasis_status oasis_pipeline_set_plan_stream(oasis_pipeline* p, int32_t where) {
   if (where != OASIS_PLAN_ON_TRANSFER && where != OASIS_PLAN_ON_PREDICTION)
     return fail(OASIS_ERR_INVALID_ARG, "%s: where = %d is neither OASIS_PLAN_ON_TRANSFER nor OASIS_PLAN_ON_PREDICTION",
                 fn, where);
+  if (where == OASIS_PLAN_ON_PREDICTION) {
+    for (int l = 0; l < p->max_layers; ++l) {
+      if (!p->is_set[l]) continue;
+      const hipError_t e = alloc_plan_ws(p, l);
+      if (e != hipSuccess) return hip_status(e, fn);
+    }
+  }
   p->plan_on_pred = where == OASIS_PLAN_ON_PREDICTION;
   return ok();
 }
@@ -313,6 +327,8 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   // layer's workspace (the slot map stays as the attention reads it); the
   // transfer stream then only copies and commits the planned rows.
   oasis::StageArgs gp = ga;
+  if (p->plan_on_pred && !p->plan_ws[layer])  // made by set_layer / set_plan_stream
+    return fail(OASIS_ERR_INVALID_ARG, "%s: layer %d has no plan workspace", fn, layer);
   if (p->plan_on_pred) {
     gp.mode = oasis::kStagePlanOnly;
     gp.ws = p->plan_ws[layer];

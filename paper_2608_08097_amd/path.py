@@ -139,6 +139,13 @@ class DecodePath:
             st.layer_id, st.pipe = lid, self._pipe
         return lid
 
+    def set_plan_on_prediction(self, on: bool):
+        """Plan the native issuer's transfers in the top-K kernel (True) or the staging kernel
+        (False), from the next step on."""
+        self.plan_on_prediction = bool(on)
+        if self._pipe is not None:
+            L.oasis_pipeline_set_plan_stream(self._pipe, L.PLAN_ON_PREDICTION if on else L.PLAN_ON_TRANSFER)
+
     def set_local_source(self, k_pages: torch.Tensor | None, v_pages: torch.Tensor | None,
                          block_table: torch.Tensor | None):
         """Refresh the local block of growing steps from these pages (bf16 [N][Hkv][B][d], device or

@@ -455,14 +455,16 @@ def test_dense_equivalence():
     assert_lse_close(st.lse.cpu().numpy(), ref_l)
 
 
-@pytest.mark.parametrize("issue", ["native", "native_plan_pred", "python"])
+@pytest.mark.parametrize("issue", ["native", "native_plan_pred", "native_plan_alternating", "python"])
 @pytest.mark.parametrize("cap", [None, 2])
 def test_pipelined_multistep(cap, issue):
     """Reasoning-style loop: AR(1) queries, one token per step, attention on the previous step's staging.
 
     With a fetch cap, later steps attend stale residents in place of the misses
     that were not admitted (paper §5.5.1), on both sides alike. ``native_plan_pred``
-    plans each transfer in the top-K kernel on the prediction stream.
+    plans each transfer in the top-K kernel on the prediction stream;
+    ``native_plan_alternating`` switches between the two streams every step (the
+    first switch comes after the layer is registered).
     """
     steps = 6
     w = make_workload("c3", num_reqs=3, ctx_args=(200, 300, 1400), steps=steps, budget=16 * 24)
@@ -494,6 +496,8 @@ def test_pipelined_multistep(cap, issue):
         note(f"pipelined step {s} cap={cap} issue={issue}")
         ctx_d, q_d = dev_i32(ctx), dev_bf16(q)
         path.build_summaries(st, ctx_d)   # summaries of blocks completed so far
+        if issue == "native_plan_alternating":
+            path.set_plan_on_prediction(s % 2 == 1)
         path.step_pipelined(st, q_d, ctx_d, s, growing=True)
         path.join()
         torch.cuda.synchronize()

@@ -23,6 +23,12 @@ the working set of consecutive steps does not sit in the 256 MB Infinity Cache
 (the host K/V tier is shared by the layers; each layer has its own query
 stream, summaries, slot map and pools).
 
+The transfer of each step is planned (delta selection, paper §4.2.3) in the
+staging kernel on the transfer stream, or with `--plan-stream prediction` in
+the top-K kernel on the prediction stream; `auto` takes the prediction stream
+for the 32-layer reasoning loop (`--workload c3`), where the transfer stream
+sets the rate, and the transfer stream otherwise.
+
 Output: one JSON line (see the fields at the end of main()).
 """
 from __future__ import annotations

@@ -201,14 +201,37 @@ def describe(c, ctx, budget, K, fetch_cap, NL):
             f"per KV head per step, AR(1) queries, {NL} rotating layer states")
 
 
+def host_cores() -> int:
+    """CPU cores this process may run on (its affinity set)."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def blas_threads():
+    """Threads of the BLAS library NumPy calls (threadpoolctl), or None if it cannot be asked."""
+    try:
+        from threadpoolctl import threadpool_info
+    except ImportError:  # pragma: no cover
+        return None
+    n = [i.get("num_threads") for i in threadpool_info() if i.get("user_api") == "blas"]
+    return n[0] if n else None
+
+
 def cpu_baseline(w, hk, hv, queries, k, fetch_cap, budget_s):
-    """Time the oracle on a bounded sample of the same step.
+    """Time the oracle on a bounded sample of the same step, on the host's own cores.
 
     Every request's working set is first filled from its step-0 prediction
     (untimed, as on the GPU); then whole-batch decode steps are timed, each
-    one scoring, top-K, capped delta staging and attention per request, until
-    the budget is spent. ``queries`` are the bf16 queries of consecutive steps.
+    one scoring, top-K, capped delta staging and attention per request. The
+    requests of a step are independent, so they run on a pool of worker
+    threads, one per host core up to the batch size, with the BLAS library
+    held to one thread per worker; a first, shorter sample runs the same
+    steps on a single thread. ``queries`` are the bf16 queries of
+    consecutive steps.
     """
+    from concurrent.futures import ThreadPoolExecutor
     from oracle import oasis_oracle as O
     try:
         from threadpoolctl import threadpool_limits
@@ -219,35 +242,59 @@ def cpu_baseline(w, hk, hv, queries, k, fetch_cap, budget_s):
     ctx = w.ctx_len(0)
     B, H, d = c.block_size, c.num_kv_heads, c.head_dim
     cap = None if fetch_cap >= k else fetch_cap
+    cores = host_cores()
+    blas_default = blas_threads()
+    workers = max(1, min(c.num_reqs, cores))
+
+    def fill(r):
+        bt, cr = w.block_table[r:r + 1], ctx[r:r + 1]
+        kmax, kmin = O.block_summaries(hk, bt, cr, B, w.NBmax)
+        s = O.block_scores(queries[0][r:r + 1], kmax, kmin, cr, H, B)
+        sel, cnt = O.select_topk(s, cr, k, B)
+        smap = np.full((1, H, k), -1, np.int32)
+        stamp = np.zeros_like(smap)
+        pk = np.zeros((1, k + 1, H, B, d), np.uint16)
+        pv = np.zeros_like(pk)
+        O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, 0, pk, pv, cr, B)
+        return (bt, cr, kmax, kmin, smap, stamp, pk, pv)
+
+    def one(r, st, step):
+        bt, cr, kmax, kmin, smap, stamp, pk, pv = st
+        qr = queries[step][r:r + 1]
+        s = O.block_scores(qr, kmax, kmin, cr, H, B)
+        sel, cnt = O.select_topk(s, cr, k, B)
+        O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, step, pk, pv, cr, B, scores=s, fetch_cap=cap)
+        O.sparse_attend(qr, pk, pv, smap, cr, B)
+
     limit = threadpool_limits(limits=1) if threadpool_limits is not None else contextlib.nullcontext()
-    with limit:
-        state = []
-        for r in range(c.num_reqs):   # setup, not timed
-            bt, cr = w.block_table[r:r + 1], ctx[r:r + 1]
-            kmax, kmin = O.block_summaries(hk, bt, cr, B, w.NBmax)
-            s = O.block_scores(queries[0][r:r + 1], kmax, kmin, cr, H, B)
-            sel, cnt = O.select_topk(s, cr, k, B)
-            smap = np.full((1, H, k), -1, np.int32)
-            stamp = np.zeros_like(smap)
-            pk = np.zeros((1, k + 1, H, B, d), np.uint16)
-            pv = np.zeros_like(pk)
-            O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, 0, pk, pv, cr, B)
-            state.append((bt, cr, kmax, kmin, smap, stamp, pk, pv))
-        steps, spent = 0, 0.0
-        while spent < budget_s and steps + 1 < len(queries):
-            steps += 1
-            for r, (bt, cr, kmax, kmin, smap, stamp, pk, pv) in enumerate(state):
-                qr = queries[steps][r:r + 1]
+    with limit, ThreadPoolExecutor(max_workers=workers) as ex:
+        state = list(ex.map(fill, range(c.num_reqs)))   # setup, not timed
+        step = 0
+
+        def sample(seconds, pool):
+            nonlocal step
+            steps, spent = 0, 0.0
+            while spent < seconds and step + 1 < len(queries):
+                step += 1
                 t0 = time.perf_counter()
-                s = O.block_scores(qr, kmax, kmin, cr, H, B)
-                sel, cnt = O.select_topk(s, cr, k, B)
-                O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, steps, pk, pv, cr, B, scores=s, fetch_cap=cap)
-                O.sparse_attend(qr, pk, pv, smap, cr, B)
+                if pool is None:
+                    for r, st in enumerate(state):
+                        one(r, st, step)
+                else:
+                    list(pool.map(lambda r: one(r, state[r], step), range(c.num_reqs)))
                 spent += time.perf_counter() - t0
-    return {"value": steps / spent, "unit": "steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} whole decode steps of all {c.num_reqs} requests (scores, top-K, delta staging "
-                      f"with fetch cap {fetch_cap}, attention; after an untimed initial fill) in float64 NumPy "
-                      f"on 1 thread, {spent:.1f} s"}
+                steps += 1
+            return steps, spent
+
+        n1, t1 = sample(budget_s / 3, None)
+        nw, tw = sample(2 * budget_s / 3, ex)
+    return {"value": nw / tw, "unit": "steps/s", "cores": workers, "kind": "oracle",
+            "host_cores": cores, "blas_threads_per_worker": 1, "blas_threads_default": blas_default,
+            "value_1_thread": n1 / t1,
+            "sample": f"whole decode steps of all {c.num_reqs} requests (scores, top-K, delta staging with fetch "
+                      f"cap {fetch_cap}, attention; after an untimed initial fill) in float64 NumPy: {nw} steps in "
+                      f"{tw:.1f} s with the requests on {workers} worker threads (host has {cores} cores), then "
+                      f"the rate of {n1} earlier steps on 1 thread ({t1:.1f} s)"}
 
 
 def main():
@@ -681,22 +728,16 @@ def isolated(P, torch, path, layers, qs, ctx_d, iters=64):
 
 
 def dense_attention(P, torch, w, hk_t, hv_t, ctx_d, d, c, iters=20):
-    """Same attention kernel over the whole context resident in HBM (identity slot map)."""
-    R, H, B, D = c.num_reqs, c.num_kv_heads, c.block_size, c.head_dim
-    nb = w.NBmax
-    bt = torch.from_numpy(w.block_table.astype(np.int64))
-    pool_k = torch.empty((R, nb, H, B, D), dtype=torch.bfloat16, device="cuda")
-    pool_v = torch.empty((R, nb, H, D, B), dtype=torch.bfloat16, device="cuda")
-    for r in range(R):
-        pages = bt[r]
-        pool_k[r].copy_(hk_t.view(torch.bfloat16)[pages].cuda())
-        pool_v[r].copy_(hv_t.view(torch.bfloat16)[pages].cuda().transpose(-1, -2))
-    ks = nb - 1
-    smap = torch.arange(ks, dtype=torch.int32, device="cuda").repeat(R * H).view(R, H, ks).contiguous()
-    out = torch.empty((R, c.T, c.num_q_heads, D), dtype=torch.bfloat16, device="cuda")
-    lse = torch.empty((R, c.T, c.num_q_heads), dtype=torch.float32, device="cuda")
+    """Same attention kernel over the whole context resident in HBM (every candidate block in the
+    slot of its own id, the local block in the last slot; `tests/test_gpu_fullsize.py` checks this
+    exact call against the oracle's dense attention)."""
+    from paper_2608_08097_amd.path import dense_working_set
+    D = c.head_dim
+    pool_k, pool_v, smap, ks = dense_working_set(hk_t, hv_t, w.block_table, w.ctx_len(0))
+    out = torch.empty((c.num_reqs, c.T, c.num_q_heads, D), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((c.num_reqs, c.T, c.num_q_heads), dtype=torch.float32, device="cuda")
     ws = torch.zeros(P.oasis_attn_workspace_bytes(d, c.T, ks), dtype=torch.uint8, device="cuda")
-    q = torch.randn((R, c.T, c.num_q_heads, D), device="cuda").to(torch.bfloat16)
+    q = torch.from_numpy(w.queries(0).view(np.int16)).cuda().view(torch.bfloat16)
     for _ in range(3):
         P.oasis_sparse_decode_attn(d, q, c.T, pool_k, pool_v, smap, ks, ctx_d, None, out, lse, ws)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -706,10 +747,12 @@ def dense_attention(P, torch, w, hk_t, hv_t, ctx_d, d, c, iters=20):
     e1.record()
     torch.cuda.synchronize()
     us = 1000.0 * e0.elapsed_time(e1) / iters
-    nbytes = R * H * int(ctx_d[0].item()) * 2 * D * 2
+    tokens = int(w.ctx_len(0).sum())
+    nbytes = c.num_kv_heads * tokens * 2 * D * 2
     del pool_k, pool_v
     return {"avg_us": round(us, 2), "algorithmic_bytes": nbytes, "achieved_GBs": round(nbytes / (us * 1e3), 1),
-            "frac": round(nbytes / (us * 1e3) / HBM_PEAK_GBS, 4), "tokens_per_head": int(ctx_d[0].item())}
+            "frac": round(nbytes / (us * 1e3) / HBM_PEAK_GBS, 4), "tokens_per_head": int(w.ctx_len(0).max()),
+            "parity": "tests/test_gpu_fullsize.py::test_fullsize_dense_c4"}
 
 
 if __name__ == "__main__":

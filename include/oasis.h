@@ -18,9 +18,16 @@
  *
  * General conventions
  * -------------------
- * - Every pointer is owned by the caller. The library allocates no memory; the
- *   scratch the attention call needs is a caller-provided workspace whose
- *   size comes from oasis_attn_workspace_bytes.
+ * - Every pointer is owned by the caller. The single-call entry points
+ *   (oasis_build_summaries ... oasis_sparse_decode_attn) allocate no memory;
+ *   the scratch the attention call needs is a caller-provided workspace whose
+ *   size comes from oasis_attn_workspace_bytes. The step issuer does allocate,
+ *   outside its steps: oasis_pipeline_create (its counter array, and the two
+ *   background streams unless the caller passes them), oasis_pipeline_set_layer
+ *   and oasis_pipeline_set_plan_stream (a plan workspace per layer when the plan
+ *   runs on the prediction stream) and oasis_pipeline_profile_begin (timing
+ *   events); oasis_pipeline_destroy frees all of it. oasis_pipeline_step and
+ *   oasis_pipeline_join allocate nothing.
  * - Calls are asynchronous on `stream` (a hipStream_t passed as void*, NULL =
  *   the null stream). They return once the kernels are enqueued.
  * - Host-side checks (null pointers, supported sizes, workspace size) return
@@ -55,8 +62,10 @@
  *   slot_map     int32 [R][Hkv][k]          resident logical block per slot, -1 = free (§4.3)
  *   slot_stamp   int32 [R][Hkv][k]          decode step at which the slot was last selected (§4.2.3)
  *   pool_k       bf16 [R][k+1][Hkv][B][d]   HBM working set, keys, token-major per head
- *   pool_v       bf16 [R][k+1][Hkv][d][B]   HBM working set, values, transposed per head
- *                (slot k of both pools holds the active local block)
+ *   pool_v       bf16 [R][k+1][Hkv][d][B]   HBM working set, values, TRANSPOSED per head:
+ *                d x B, unlike the token-major K pool and the host pages (the
+ *                staging kernel transposes while it copies); slot k of both
+ *                pools holds the active local block
  *   out          bf16 [R][T][Hq][d]
  *   lse          fp32 [R][T][Hq]            natural-log log-sum-exp of the scaled logits
  */
@@ -157,9 +166,9 @@ OASIS_API oasis_status oasis_copy_blocks(const oasis_dims* dims, const uint16_t*
                                const int32_t* ctx_len, int32_t max_blocks, void* stream);
 
 /*
- * Block importance from the lookahead (draft) queries (paper §4.2.1: each
- * draft query scans the compressed keys and ranks all logical blocks
- * independently per KV head). For row q of query head qh, the Quest upper
+ * Block importance from the lookahead (draft) queries (paper §4.2.1: the
+ * prediction reads only the compressed keys and ranks every logical block,
+ * separately per KV head). For row q of query head qh, the Quest upper
  * bound of block b is  sum_d max(q_d * kmin_d, q_d * kmax_d); the score of
  * (r, h, b) is the maximum of that bound over the rows t in [first_draft,
  * first_draft + num_draft) and the G query heads of KV head h. Scores of
@@ -192,9 +201,9 @@ OASIS_API oasis_status oasis_select_topk(const oasis_dims* dims, const float* sc
  * Delta selection + KV transfer into the HBM working set (paper §4.2.3: resident
  * hits stay and move no bytes; non-selected residents are evicted least-recently-
  * selected first; each admitted miss is paired with one eviction target; §4.3:
- * the head-wise slot map records which logical block every slot holds; §5.1: a
- * gather kernel reads the selected block-head entries from pinned host memory
- * over PCIe and writes them into the resident GPU pages).
+ * the head-wise slot map records which logical block every slot holds; §5.1:
+ * the copy is a GPU kernel that pulls each admitted (block, KV head) entry out
+ * of pinned host memory across PCIe into its pool slot).
  *
  * For every (r, h), with S = sel[r][h][0..sel_count) (ascending, as produced by
  * oasis_select_topk): misses = S minus the resident blocks; admitted = all

@@ -166,9 +166,9 @@ def block_scores(q, kmax, kmin, ctx_len, num_kv_heads: int, block_size: int,
                  first_draft: int = 1, num_draft: int | None = None):
     """Importance of every candidate block for every (request, KV head).
 
-    Paper §4.2.1: each draft query scans the compressed keys and ranks all
-    logical blocks independently for every KV head, covering the whole context
-    without restoring any key. The importance of a block to one query row is
+    Paper §4.2.1: the prediction reads only the compressed keys, so every
+    logical block of the context gets a rank, separately per KV head, and no
+    full key is brought back for it. The importance of a block to one query row is
     the Quest upper bound on that row's dot product with any key of the block
     (reading R1): for every coordinate take the larger of q_d * kmin_d and
     q_d * kmax_d, and add the coordinates up (no 1/sqrt(d): the ranking does

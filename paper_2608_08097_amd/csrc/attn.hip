@@ -10,9 +10,11 @@
 // softmax. The waves are merged through LDS; with one split the workgroup
 // writes the bf16 outputs and the log-sum-exp itself, otherwise each split
 // writes one partial (unnormalised output, running max, running sum) per row
-// and a second kernel merges the splits. (A last-arriving-workgroup merge in
-// the same kernel measured slower on MI355X: its agent-scope release/acquire
-// costs more than the second launch.)
+// and a second kernel merges the splits. (A merge by the last-arriving
+// workgroup of a head inside the same kernel needs an agent-scope release
+// per workgroup, which on MI355X writes back the XCD's L2; measured on a
+// 256-workgroup stand-in, that cost 14.8 us per call against 2.6 us for the
+// second launch.)
 //
 // One 32-token unit for one 16-row tile:
 //   S^T (tokens x rows) = K (tokens x d) . Q^T (d x rows): 2 token tiles x
@@ -30,7 +32,6 @@
 #include "oasis_internal.h"
 
 namespace oasis {
-
 namespace {
 
 constexpr int kW = 4;  // waves per workgroup
@@ -54,12 +55,10 @@ __device__ __forceinline__ bool map_workgroup(int wg, int nrh, int nsplit, int& 
   return rh < nrh;
 }
 
-// K and V registers of one 32-token unit, plus the token counts of its two
-// slots (0 = not attended).
+// K and V registers of one 32-token unit (the operands of its MFMAs).
 struct UnitRegs {
   u32x4 k[2][4];
   u32x4 v[8];
-  int n0, n1;
 };
 
 // Unit u (wave-uniform) covers slots s0 = 2u, s1 = 2u + 1 at B = 16 or slot u
@@ -73,9 +72,8 @@ struct UnitRegs {
 // the same number of loads on every path keeps the compiler's wait counts
 // exact, so waiting for the current unit never drains the prefetched one.
 template <int BS>
-__device__ __forceinline__ void load_unit(UnitRegs& ur, int u, int ks, int local_len, const int32_t* smap,
-                                          const uint16_t* pk, const uint16_t* pv, long long slot_elems, int g,
-                                          int i) {
+__device__ __forceinline__ void load_unit(UnitRegs& ur, int u, int ks, const uint16_t* pk, const uint16_t* pv,
+                                          long long slot_elems, int g, int i) {
   const bool real = u >= 0;
   const int s0 = real ? (BS == 16 ? 2 * u : u) : ks;
   const int s1raw = real ? (BS == 16 ? 2 * u + 1 : ks + 1) : ks + 1;
@@ -97,21 +95,33 @@ __device__ __forceinline__ void load_unit(UnitRegs& ur, int u, int ks, int local
   const uint16_t* vsrc = BS == 16 ? ((g < 2 ? v0 : v1) + (g & 1) * 8) : (v0 + 8 * g);
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) ur.v[dt] = ldg16(vsrc + (long long)(dt * 16 + i) * BS);
-  // token counts of the two slots (0 = not attended)
-  ur.n0 = !real ? 0 : (s0 < ks ? (smap[s0] >= 0 ? BS : 0) : (s0 == ks ? local_len : 0));
-  ur.n1 = (BS == 16 && real) ? (s1raw < ks ? (smap[s1raw] >= 0 ? BS : 0) : (s1raw == ks ? local_len : 0)) : 0;
+}
+
+// Attended tokens of the two slots of unit u (u < 0: none): a slot below k_slots
+// counts B tokens when bit `bit` (first slot) / `bit + 1` (second slot, B = 16)
+// of the validity mask is set; slot k_slots is the local block.
+template <int BS>
+__device__ __forceinline__ void unit_counts(int u, int ks, int local_len, uint64_t vmask, int bit, int& n0,
+                                            int& n1) {
+  const int s0 = BS == 16 ? 2 * u : u;
+  const int s1 = s0 + 1;
+  n0 = u < 0 ? 0 : (s0 < ks ? (((vmask >> bit) & 1) ? BS : 0) : (s0 == ks ? local_len : 0));
+  n1 = (BS == 16 && u >= 0) ? (s1 < ks ? (((vmask >> (bit + 1)) & 1) ? BS : 0) : (s1 == ks ? local_len : 0)) : 0;
+}
+
+// Tokens of the unit that lane (g, i) scores: 8g .. 8g+7 of the unit (slot 0 holds
+// unit tokens 0 .. B-1). The first `keep` of them are attended (0 .. 8).
+template <int BS>
+__device__ __forceinline__ int lane_keep(int n0, int n1, int g) {
+  const int cnt = BS == 16 ? (g < 2 ? n0 : n1) : n0;
+  const int k = cnt - (BS == 16 ? (g & 1) * 8 : 8 * g);
+  return k < 0 ? 0 : (k > 8 ? 8 : k);
 }
 
 // Zero the V values of tokens that are not attended (their probability is 0,
-// but 0 * NaN would poison the accumulator). Only lanes whose 8 tokens are not
-// all attended (a free slot, the tail of the local block) do any work; in a
-// full unit the whole wave skips it.
-template <int BS>
-__device__ __forceinline__ void mask_unit_v(UnitRegs& ur, int g) {
-  const int cnt = BS == 16 ? (g < 2 ? ur.n0 : ur.n1) : ur.n0;
-  const int t0 = BS == 16 ? (g & 1) * 8 : 8 * g;
-  const int keep = cnt - t0;
-  if (keep >= 8) return;
+// but 0 * NaN would poison the accumulator). Lane (g, i) holds V^T of the same
+// 8 tokens it scores; only lanes with keep < 8 change anything.
+__device__ __forceinline__ void mask_unit_v(UnitRegs& ur, int keep) {
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt)
 #pragma unroll
@@ -131,20 +141,15 @@ __device__ __forceinline__ void mask_unit_v(UnitRegs& ur, int g) {
 // first unit has been seen) are the row maxima exchanged across lanes and the
 // accumulators rescaled. Probabilities stay below 2^kLazyTh, far inside the
 // fp32 range, and the result is the same softmax.
+//
+// `partial` (wave-uniform) is set when some lane has keep < 8: only then are
+// unattended scores set to -inf; a fully attended unit skips that work.
 constexpr float kLazyTh = 8.f;
 
 template <int NT, int BS>
-__device__ __forceinline__ void process_unit(const UnitRegs& cur, const bf16x8 (&qb)[NT][4], float (&m_ref)[NT],
-                                             float (&l_part)[NT], f32x4 (&acc)[NT][8], int g, float scale_log2) {
-  // validity of the 8 unit tokens 8g + 4*tau + j this lane scores
-  bool valid[2][4];
-#pragma unroll
-  for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int tok = 8 * g + 4 * tau + j;
-      valid[tau][j] = BS == 16 ? (tok < 16 ? tok < cur.n0 : (tok - 16) < cur.n1) : tok < cur.n0;
-    }
+__device__ __forceinline__ void process_unit(const UnitRegs& cur, int keep, bool partial, const bf16x8 (&qb)[NT][4],
+                                             float (&m_ref)[NT], float (&l_part)[NT], f32x4 (&acc)[NT][8],
+                                             float scale_log2) {
 #pragma unroll
   for (int v = 0; v < NT; ++v) {
     f32x4 sc[2];
@@ -157,15 +162,13 @@ __device__ __forceinline__ void process_unit(const UnitRegs& cur, const bf16x8 (
       sc[tau] = s4;
     }
     float x[8];
-    float lmax = -INFINITY;
 #pragma unroll
-    for (int tau = 0; tau < 2; ++tau)
+    for (int e = 0; e < 8; ++e) x[e] = sc[e >> 2][e & 3] * scale_log2;
+    if (partial) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float z = valid[tau][j] ? sc[tau][j] * scale_log2 : -INFINITY;
-        x[4 * tau + j] = z;
-        lmax = fmaxf(lmax, z);
-      }
+      for (int e = 0; e < 8; ++e) x[e] = e < keep ? x[e] : -INFINITY;
+    }
+    const float lmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])), fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
     if (__builtin_amdgcn_ballot_w64(lmax > m_ref[v] + kLazyTh)) {
       float rmax = fmaxf(lmax, __shfl_xor(lmax, 16));
       rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
@@ -205,6 +208,26 @@ __device__ __forceinline__ void write_output(const AttnArgs& a, int r, int h, in
   if (c4 == 0 && a.lse) a.lse[orow] = L > 0.f ? (M + __log2f(L)) * 0.69314718055994531f : -INFINITY;
 }
 
+// Slot-map validity of the wave's units t0 .. t0 + kChunk - 1 (unit t of the wave is
+// u_first + t * kW): lane l reads the map entry of slot l % 2 of unit t0 + l / 2
+// (B = 16) or of unit t0 + l (B = 32); ballot(slot < k_slots && entry >= 0) is then
+// the mask unit_counts reads (bit 2j + e or j), so the unit loop loads no slot map.
+// The load is split from the test: it is issued unconditionally (index clamped
+// into the map; with k_slots = 0, where the map may be NULL, from `fallback`,
+// any valid int, whose value the slot test then ignores), so that nothing waits
+// for it until the mask is needed.
+template <int BS>
+__device__ __forceinline__ int unit_slot(int u_first, int t0, int lane) {
+  const int j = BS == 16 ? lane >> 1 : lane;
+  return BS == 16 ? 2 * (u_first + (t0 + j) * kW) + (lane & 1) : u_first + (t0 + j) * kW;
+}
+__device__ __forceinline__ int map_load(const int32_t* smap, int ks, int slot, const int32_t* fallback) {
+  return *(ks > 0 ? smap + (slot < ks ? slot : ks - 1) : fallback);
+}
+__device__ __forceinline__ uint64_t map_mask(int ks, int slot, int entry) {
+  return __builtin_amdgcn_ballot_w64(slot < ks && entry >= 0);
+}
+
 template <int NT, int BS>
 __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
@@ -216,8 +239,26 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   if (!map_workgroup(blockIdx.x, nrh, a.nsplit, rh, split)) return;
   const int r = rh / a.Hkv;
   const int h = rh - r * a.Hkv;
-  const Ctx c = ctx_blocks(a.ctx_len[r], BS, a.NBmax);
   const int ks = a.k_slots;
+  const long long slot_elems = (long long)a.Hkv * BS * kHeadDim;
+  const long long head_off = (long long)h * BS * kHeadDim;
+  const uint16_t* pk = a.pool_k + (long long)r * (ks + 1) * slot_elems + head_off;
+  const uint16_t* pv = a.pool_v + (long long)r * (ks + 1) * slot_elems + head_off;
+  const int32_t* smap = a.slot_map + (long long)rh * ks;
+  const int u_begin = split * a.units_per_split;
+  const int u_end = min(a.n_units, u_begin + a.units_per_split);
+  // unit t of this wave is u_first + t * kW, t < nt
+  const int u_first = u_begin + wave;
+  const int nt = u_first < u_end ? (u_end - u_first + kW - 1) / kW : 0;
+  auto unit = [&](int t) { return t < nt ? u_first + t * kW : -1; };
+  constexpr int kChunk = BS == 16 ? 32 : 64;  // units per validity mask
+  auto bit_of = [&](int t) { return BS == 16 ? 2 * (t & (kChunk - 1)) : (t & (kChunk - 1)); };
+
+  // The first unit's loads go out before anything else, so that no wave starts
+  // by waiting for a scalar or query load; the queries, the slot map and the
+  // context length follow.
+  UnitRegs ua, ub;
+  load_unit<BS>(ua, unit(0), ks, pk, pv, slot_elems, g, i);
 
   // Q^T operand: lane (g, i) holds row v*16 + i of tile v, dims st*32 + 8g .. +8.
   bf16x8 qb[NT][4];
@@ -225,9 +266,9 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   for (int v = 0; v < NT; ++v) {
     const int row = v * 16 + i;
     if (row < a.rows) {
-      const int t = row / a.G;
-      const int qh = h * a.G + (row - t * a.G);
-      const uint16_t* qrow = a.q + (((long long)r * a.T + t) * a.Hq + qh) * kHeadDim;
+      const int tq = row / a.G;
+      const int qh = h * a.G + (row - tq * a.G);
+      const uint16_t* qrow = a.q + (((long long)r * a.T + tq) * a.Hq + qh) * kHeadDim;
 #pragma unroll
       for (int st = 0; st < 4; ++st) qb[v][st] = as_bf16x8(ldg16(qrow + st * 32 + g * 8));
     } else {
@@ -235,12 +276,12 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
       for (int st = 0; st < 4; ++st) qb[v][st] = as_bf16x8(u32x4{0, 0, 0, 0});
     }
   }
-
-  const long long slot_elems = (long long)a.Hkv * BS * kHeadDim;
-  const long long head_off = (long long)h * BS * kHeadDim;
-  const uint16_t* pk = a.pool_k + (long long)r * (ks + 1) * slot_elems + head_off;
-  const uint16_t* pv = a.pool_v + (long long)r * (ks + 1) * slot_elems + head_off;
-  const int32_t* smap = a.slot_map + (long long)rh * ks;
+  const int map_slot = unit_slot<BS>(u_first, 0, lane);
+  int map_entry = map_load(smap, ks, map_slot, a.ctx_len + r);
+  // a vector load (relaxed atomic) whose value is pinned to a VGPR until the
+  // next unit's loads are out, so that the wait for it comes after them
+  int ctx_raw = __hip_atomic_load(a.ctx_len + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  __builtin_amdgcn_sched_barrier(0);
 
   float m_run[NT], l_run[NT];  // row reference maximum (log2 units) and this lane's partial sum
   f32x4 acc[NT][8];
@@ -252,35 +293,51 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
     for (int dt = 0; dt < 8; ++dt) acc[v][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  const int u_begin = split * a.units_per_split;
-  const int u_end = min(a.n_units, u_begin + a.units_per_split);
+  int local_len = 0;
+  // One unit: counts from the mask (reloaded at the first unit of every chunk
+  // after the first), V of unattended tokens cleared, then the online softmax.
+  uint64_t vmask = 0;
+  auto run = [&](UnitRegs& cur, int t) {
+    if (t > 0 && (t & (kChunk - 1)) == 0) {
+      const int slot = unit_slot<BS>(u_first, t, lane);
+      vmask = map_mask(ks, slot, map_load(smap, ks, slot, a.ctx_len + r));
+    }
+    int n0, n1;
+    unit_counts<BS>(unit(t), ks, local_len, vmask, bit_of(t), n0, n1);
+    const int keep = lane_keep<BS>(n0, n1, g);
+    const bool partial = __builtin_amdgcn_ballot_w64(keep < 8) != 0;
+    if (partial) mask_unit_v(cur, keep);
+    process_unit<NT, BS>(cur, keep, partial, qb, m_run, l_run, acc, a.scale_log2);
+  };
 
   // With few row tiles the next unit's K/V loads are issued before the current
   // unit is computed (one exposed memory latency per wave, not per unit); with
-  // many row tiles the registers go to the accumulators instead.
+  // many row tiles the registers go to the accumulators instead. Loads past the
+  // wave's last unit are placeholders on the local slot (cache-resident), so the
+  // compiler's wait counts stay exact.
   constexpr bool kPrefetch = NT <= 2;
-  int u = u_begin + wave;
+  auto settle = [&]() {  // the map entries and the context length are in
+    asm volatile("" : "+v"(map_entry), "+v"(ctx_raw));
+    vmask = map_mask(ks, map_slot, map_entry);
+    local_len = ctx_blocks(ctx_raw, BS, a.NBmax).local_len;
+  };
   if (kPrefetch) {
-    // two register buffers used alternately (no copies between them)
-    UnitRegs ua, ub;
-    load_unit<BS>(ua, u < u_end ? u : -1, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
-    while (u < u_end) {
-      load_unit<BS>(ub, u + kW < u_end ? u + kW : -1, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
-      mask_unit_v<BS>(ua, g);
-      process_unit<NT, BS>(ua, qb, m_run, l_run, acc, g, a.scale_log2);
-      u += kW;
-      if (u >= u_end) break;
-      load_unit<BS>(ua, u + kW < u_end ? u + kW : -1, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
-      mask_unit_v<BS>(ub, g);
-      process_unit<NT, BS>(ub, qb, m_run, l_run, acc, g, a.scale_log2);
-      u += kW;
+    load_unit<BS>(ub, unit(1), ks, pk, pv, slot_elems, g, i);
+    __builtin_amdgcn_sched_barrier(0);  // both units' loads are issued before the first wait
+    settle();
+    for (int t = 0; t < nt;) {
+      run(ua, t);
+      if (++t >= nt) break;
+      load_unit<BS>(ua, unit(t + 1), ks, pk, pv, slot_elems, g, i);
+      run(ub, t);
+      if (++t >= nt) break;
+      load_unit<BS>(ub, unit(t + 1), ks, pk, pv, slot_elems, g, i);
     }
   } else {
-    for (; u < u_end; u += kW) {
-      UnitRegs cur;
-      load_unit<BS>(cur, u, ks, c.local_len, smap, pk, pv, slot_elems, g, i);
-      mask_unit_v<BS>(cur, g);
-      process_unit<NT, BS>(cur, qb, m_run, l_run, acc, g, a.scale_log2);
+    settle();
+    for (int t = 0; t < nt; ++t) {
+      if (t > 0) load_unit<BS>(ua, unit(t), ks, pk, pv, slot_elems, g, i);
+      run(ua, t);
     }
   }
   // row sums: add the partial sums of the four lanes of every row
@@ -291,15 +348,17 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   }
 
   // ---- merge the waves of this workgroup through LDS -----------------------
-  // Row maxima first; every wave rescales its accumulators to them and writes
-  // them to a slice (kSlices slices; with fewer slices than waves the other
-  // waves add into them in a second round); then every thread sums the slices
-  // of some (row, dimension) entries in a fixed order.
+  // Each wave publishes its row maxima and sums; every lane then reads those of
+  // all waves for its rows (all reads issued before any is used, no branch on
+  // them), rescales its accumulators to the merged maximum and writes them to
+  // its slice (kSlices slices; with fewer slices than waves the other waves add
+  // into them in a second round); finally every thread sums the slices of a few
+  // (row, 4-dimension) positions, all their reads again issued at once.
   constexpr int kRows = NT * 16;
   constexpr int kPad = kHeadDim + 4;
   constexpr int kSlices = NT <= 4 ? kW : 2;  // LDS: kSlices * kRows * kPad floats <= 160 KiB
-  __shared__ float s_m[kW][kRows], s_l[kW][kRows];
-  __shared__ float s_o[kSlices][kRows][kPad];
+  __shared__ float s_m[kW][kRows], s_l[kW][kRows], s_ml[2][kRows];
+  __shared__ __align__(16) float s_o[kSlices][kRows][kPad];
   if (g == 0) {
 #pragma unroll
     for (int v = 0; v < NT; ++v) {
@@ -311,12 +370,25 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
 #pragma unroll
   for (int v = 0; v < NT; ++v) {
     const int row = v * 16 + i;
-    float M = -INFINITY;
+    float mw[kW], lw[kW];
 #pragma unroll
-    for (int w = 0; w < kW; ++w) M = fmaxf(M, s_m[w][row]);
-    const float f = M == -INFINITY ? 0.f : fast_exp2(m_run[v] - M);
+    for (int w = 0; w < kW; ++w) {
+      mw[w] = s_m[w][row];
+      lw[w] = s_l[w][row];
+    }
+    float M = mw[0];
+#pragma unroll
+    for (int w = 1; w < kW; ++w) M = fmaxf(M, mw[w]);
+    float L = 0.f;
+#pragma unroll
+    for (int w = 0; w < kW; ++w) L += mw[w] == -INFINITY ? 0.f : lw[w] * fast_exp2(mw[w] - M);
+    const float f = m_run[v] == -INFINITY ? 0.f : fast_exp2(m_run[v] - M);
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) acc[v][dt] *= f;
+    if (wave == 0 && g == 0) {
+      s_ml[0][row] = M;
+      s_ml[1][row] = L;
+    }
   }
 #pragma unroll
   for (int round = 0; round < kW / kSlices; ++round) {
@@ -326,18 +398,8 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
       for (int v = 0; v < NT; ++v)
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
-          float* dst = &s_o[sl][v * 16 + i][dt * 16 + 4 * g];
-          f32x4 val = acc[v][dt];
-          if (round > 0) {
-            val[0] += dst[0];
-            val[1] += dst[1];
-            val[2] += dst[2];
-            val[3] += dst[3];
-          }
-          dst[0] = val[0];
-          dst[1] = val[1];
-          dst[2] = val[2];
-          dst[3] = val[3];
+          f32x4* dst = reinterpret_cast<f32x4*>(&s_o[sl][v * 16 + i][dt * 16 + 4 * g]);
+          *dst = round > 0 ? *dst + acc[v][dt] : acc[v][dt];
         }
     }
     __syncthreads();
@@ -345,31 +407,29 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
 
   const int nsplit = a.nsplit;
   const long long pbase = ((long long)rh * nsplit + split) * a.rows;
-  // (row, 4-dimension group) entries of this split: max over waves, rescale, sum
-  for (int idx = threadIdx.x; idx < a.rows * (kHeadDim / 4); idx += kW * 64) {
-    const int row = idx / (kHeadDim / 4);
-    const int c4 = idx - row * (kHeadDim / 4);
-    float M = -INFINITY;
+  constexpr int kPer = (kRows * (kHeadDim / 4) + kW * 64 - 1) / (kW * 64);  // positions per thread
+  const int npos = a.rows * (kHeadDim / 4);
+  f32x4 o[kPer];
 #pragma unroll
-    for (int w = 0; w < kW; ++w) M = fmaxf(M, s_m[w][row]);
-    f32x4 o = {0.f, 0.f, 0.f, 0.f};
-    float L = 0.f;
-    if (M != -INFINITY) {
+  for (int j = 0; j < kPer; ++j) {
+    const int pos = threadIdx.x + j * kW * 64;
+    const int row = (pos < npos ? pos : 0) >> 5;
+    const int c4 = pos & 31;
+    o[j] = *reinterpret_cast<const f32x4*>(&s_o[0][row][c4 * 4]);
 #pragma unroll
-      for (int w = 0; w < kW; ++w) L += s_m[w][row] == -INFINITY ? 0.f : s_l[w][row] * fast_exp2(s_m[w][row] - M);
+    for (int sl = 1; sl < kSlices; ++sl) o[j] += *reinterpret_cast<const f32x4*>(&s_o[sl][row][c4 * 4]);
+  }
 #pragma unroll
-      for (int sl = 0; sl < kSlices; ++sl) {
-        const float* src = &s_o[sl][row][c4 * 4];
-        o[0] += src[0];
-        o[1] += src[1];
-        o[2] += src[2];
-        o[3] += src[3];
-      }
-    }
+  for (int j = 0; j < kPer; ++j) {
+    const int pos = threadIdx.x + j * kW * 64;
+    if (pos >= npos) break;
+    const int row = pos >> 5;
+    const int c4 = pos & 31;
+    const float M = s_ml[0][row], L = s_ml[1][row];
     if (nsplit == 1) {  // the only split: finish here
-      write_output(a, r, h, row, c4, o, M, L);
+      write_output(a, r, h, row, c4, o[j], M, L);
     } else {
-      *reinterpret_cast<f32x4*>(a.part_o + (pbase + row) * kHeadDim + c4 * 4) = o;
+      *reinterpret_cast<f32x4*>(a.part_o + (pbase + row) * kHeadDim + c4 * 4) = o[j];
       if (c4 == 0) {
         a.part_ml[(pbase + row) * 2 + 0] = M;
         a.part_ml[(pbase + row) * 2 + 1] = L;
@@ -378,36 +438,42 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   }
 }
 
-// Merge of the splits: one workgroup per (row, request x KV head), one thread
-// per dimension; all partial loads of a thread are issued before any is used
-// (nsplit <= kMaxSplits).
+// Merge of the NS splits: one workgroup per (row, request x KV head), one thread
+// per dimension; every thread issues its NS partial loads and the row's NS
+// (max, sum) pairs at once. Workgroup ids are dealt so that the head's id % 8,
+// which places its splits on one XCD, places its merge there too: the partials
+// are read from the L2 that holds them.
+template <int NS>
 __global__ __launch_bounds__(kHeadDim) void attn_merge_kernel(AttnArgs a) {
-  const int row = blockIdx.x;
-  const int rh = blockIdx.y;
+  const int nrh = a.R * a.Hkv;
+  const int wg = blockIdx.x;
+  const int local = wg >> 3;
+  const int rh_local = local / a.rows;
+  const int row = local - rh_local * a.rows;
+  const int rh = rh_local * 8 + (wg & 7);
+  if (rh >= nrh) return;
   const int d = threadIdx.x;
   const int r = rh / a.Hkv;
   const int h = rh - r * a.Hkv;
-  const long long base = (long long)rh * a.nsplit * a.rows + row;
-  float ms[kMaxSplits], ls[kMaxSplits], os[kMaxSplits];
+  const long long base = (long long)rh * NS * a.rows + row;
+  float ms[NS], ls[NS], os[NS];
 #pragma unroll
-  for (int s = 0; s < kMaxSplits; ++s) {
+  for (int s = 0; s < NS; ++s) {
     const long long idx = base + (long long)s * a.rows;
-    const bool live = s < a.nsplit;
-    ms[s] = live ? a.part_ml[idx * 2] : -INFINITY;
-    ls[s] = live ? a.part_ml[idx * 2 + 1] : 0.f;
-    os[s] = live ? a.part_o[idx * kHeadDim + d] : 0.f;
+    ms[s] = a.part_ml[idx * 2];
+    ls[s] = a.part_ml[idx * 2 + 1];
+    os[s] = a.part_o[idx * kHeadDim + d];
   }
-  float M = -INFINITY;
+  float M = ms[0];
 #pragma unroll
-  for (int s = 0; s < kMaxSplits; ++s) M = fmaxf(M, ms[s]);
+  for (int s = 1; s < NS; ++s) M = fmaxf(M, ms[s]);
+  // a split with no attended token (max -inf) weighs 0; with none at all, L = 0
   float L = 0.f, o = 0.f;
-  if (M != -INFINITY) {
 #pragma unroll
-    for (int s = 0; s < kMaxSplits; ++s) {
-      const float f = ms[s] == -INFINITY ? 0.f : fast_exp2(ms[s] - M);
-      L += ls[s] * f;
-      o += os[s] * f;
-    }
+  for (int s = 0; s < NS; ++s) {
+    const float f = ms[s] == -INFINITY ? 0.f : fast_exp2(ms[s] - M);
+    L += ls[s] * f;
+    o += os[s] * f;
   }
   const float res = L > 0.f ? o / L : 0.f;
   const int t = row / a.G;
@@ -415,6 +481,31 @@ __global__ __launch_bounds__(kHeadDim) void attn_merge_kernel(AttnArgs a) {
   const long long orow = ((long long)r * a.T + t) * a.Hq + qh;
   a.out[orow * kHeadDim + d] = (uint16_t)f32_to_bf16_bits(res);
   if (d == 0 && a.lse) a.lse[orow] = L > 0.f ? (M + __log2f(L)) * 0.69314718055994531f : -INFINITY;
+}
+
+template <int NS>
+void launch_merge_ns(const AttnArgs& a, hipStream_t s, const LaunchTiming& t, int nrh8) {
+  launch_kernel(attn_merge_kernel<NS>, dim3((unsigned)(nrh8 * a.rows)), dim3(kHeadDim), s, t, a);
+}
+
+void launch_merge(const AttnArgs& a, hipStream_t s, const LaunchTiming& t, int nrh8) {
+  switch (a.nsplit) {
+    case 2: return launch_merge_ns<2>(a, s, t, nrh8);
+    case 3: return launch_merge_ns<3>(a, s, t, nrh8);
+    case 4: return launch_merge_ns<4>(a, s, t, nrh8);
+    case 5: return launch_merge_ns<5>(a, s, t, nrh8);
+    case 6: return launch_merge_ns<6>(a, s, t, nrh8);
+    case 7: return launch_merge_ns<7>(a, s, t, nrh8);
+    case 8: return launch_merge_ns<8>(a, s, t, nrh8);
+    case 9: return launch_merge_ns<9>(a, s, t, nrh8);
+    case 10: return launch_merge_ns<10>(a, s, t, nrh8);
+    case 11: return launch_merge_ns<11>(a, s, t, nrh8);
+    case 12: return launch_merge_ns<12>(a, s, t, nrh8);
+    case 13: return launch_merge_ns<13>(a, s, t, nrh8);
+    case 14: return launch_merge_ns<14>(a, s, t, nrh8);
+    case 15: return launch_merge_ns<15>(a, s, t, nrh8);
+    default: return launch_merge_ns<kMaxSplits>(a, s, t, nrh8);
+  }
 }
 
 template <int NT, int BS>
@@ -427,8 +518,7 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t s, const LaunchTiming& t) {
                 LaunchTiming{t.start, merge ? nullptr : t.stop}, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !merge) return e;
-  launch_kernel(attn_merge_kernel, dim3((unsigned)a.rows, (unsigned)nrh), dim3(kHeadDim), s,
-                LaunchTiming{nullptr, t.stop}, a);
+  launch_merge(a, s, LaunchTiming{nullptr, t.stop}, nrh8);
   return hipGetLastError();
 }
 

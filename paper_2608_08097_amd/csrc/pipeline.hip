@@ -71,6 +71,16 @@ hipError_t signal(oasis_pipeline* p, hipStream_t s, int i, uint32_t v) {
   return hipStreamWriteValue32(s, slot(p, i), v, 0);
 }
 
+// Write counter value last + 1 on stream s and record it in *last only once the
+// write is enqueued: a failed enqueue leaves the host's value as it was, so no
+// later wait is issued for a value that nothing will write.
+hipError_t signal_next(oasis_pipeline* p, hipStream_t s, int i, uint32_t* last) {
+  const uint32_t v = *last + 1;
+  const hipError_t e = signal(p, s, i, v);
+  if (e == hipSuccess) *last = v;
+  return e;
+}
+
 hipError_t wait_for(oasis_pipeline* p, hipStream_t s, int i, uint32_t v) {
   return hipStreamWaitValue32(s, slot(p, i), v, hipStreamWaitValueGte, 0xFFFFFFFFu);
 }
@@ -351,22 +361,22 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   if (p->staged[layer]) HIP_TRY(wait_for(p, fg, sl, p->staged[layer]), fn);
   // q and ctx_len are ready on the foreground; past the wait above this also
   // means the previous transfer has finished reading sel and scores
-  HIP_TRY(signal(p, fg, kQ, ++cnt[kQ]), fn);
+  HIP_TRY(signal_next(p, fg, kQ, &cnt[kQ]), fn);
   HIP_TRY(wait_for(p, p->pred, kQ, cnt[kQ]), fn);
   if (growing) HIP_TRY(oasis::launch_stage(la, fg), fn);
   HIP_TRY(oasis::launch_attn(aa, fg, prof_timing(p, 0)), fn);
-  HIP_TRY(signal(p, fg, kAttn, ++cnt[kAttn]), fn);
+  HIP_TRY(signal_next(p, fg, kAttn, &cnt[kAttn]), fn);
   if (prev_ctx_len) HIP_TRY(oasis::launch_summaries(ua, p->pred), fn);
   HIP_TRY(oasis::launch_score(sa, p->pred, prof_timing(p, 1)), fn);
   if (p->plan_on_pred)
     HIP_TRY(oasis::launch_topk_plan(ta, gp, p->pred, prof_timing(p, 2)), fn);
   else
     HIP_TRY(oasis::launch_topk(ta, p->pred, prof_timing(p, 2)), fn);
-  HIP_TRY(signal(p, p->pred, kPred, ++cnt[kPred]), fn);
+  HIP_TRY(signal_next(p, p->pred, kPred, &cnt[kPred]), fn);
   HIP_TRY(wait_for(p, p->xfer, kPred, cnt[kPred]), fn);
   HIP_TRY(wait_for(p, p->xfer, kAttn, cnt[kAttn]), fn);  // the gather overwrites slots the attention reads
   HIP_TRY(oasis::launch_stage(ga, p->xfer, prof_timing(p, 3)), fn);
-  HIP_TRY(signal(p, p->xfer, sl, ++p->staged[layer]), fn);
+  HIP_TRY(signal_next(p, p->xfer, sl, &p->staged[layer]), fn);
   if (p->prof_ev && p->prof_n < p->prof_cap) ++p->prof_n;
   return ok();
 }
@@ -377,9 +387,9 @@ oasis_status oasis_pipeline_join(oasis_pipeline* p, void* stream) {
   hipStream_t fg = static_cast<hipStream_t>(stream);
   uint32_t* cnt = p->count;
   if (cnt[kJoinPred] >= kWrapGuard || cnt[kJoinXfer] >= kWrapGuard) HIP_TRY(reset_counters(p, fg), fn);
-  HIP_TRY(signal(p, p->pred, kJoinPred, ++cnt[kJoinPred]), fn);
+  HIP_TRY(signal_next(p, p->pred, kJoinPred, &cnt[kJoinPred]), fn);
   HIP_TRY(wait_for(p, fg, kJoinPred, cnt[kJoinPred]), fn);
-  HIP_TRY(signal(p, p->xfer, kJoinXfer, ++cnt[kJoinXfer]), fn);
+  HIP_TRY(signal_next(p, p->xfer, kJoinXfer, &cnt[kJoinXfer]), fn);
   HIP_TRY(wait_for(p, fg, kJoinXfer, cnt[kJoinXfer]), fn);
   return ok();
 }

@@ -6,9 +6,9 @@
 // admitted miss is paired with one eviction target; at most fetch_cap pairs are
 // admitted per KV head and step (§5.5.1: a fetch ratio of K), the highest-
 // scoring misses first, and all other slots stay as they are. §4.3: a per-KV-head map
-// records which logical block each GPU slot holds. §5.1: a gather kernel reads
-// the selected block-head entries from pinned host memory over PCIe and
-// writes them into the resident GPU pages.
+// records which logical block each GPU slot holds. §5.1: the copy is done by a
+// kernel on the GPU that pulls each admitted (block, KV head) entry out of
+// pinned host memory across PCIe and stores it straight into its pool slot.
 //
 // A grid of 256-thread workgroups walks the (request, KV head) pairs
 // (workgroup w takes pairs w, w + grid, ...), as many pairs per pass as the

@@ -51,6 +51,43 @@ class LayerState:
         self.slot_stamp.zero_()
 
 
+def dense_working_set(host_k: torch.Tensor, host_v: torch.Tensor, block_table, ctx_len, device="cuda"):
+    """Working set that holds every block of every request: the dense comparison of the budget sweep
+    (§5.2: the budget is the sparsification threshold; a budget that covers the context is dense
+    attention), run through the same attention entry point as the sparse path.
+
+    ``block_table`` / ``ctx_len`` are host int arrays ([R][NBmax], [R]). Returns (pool_k, pool_v,
+    slot_map, k_slots) with k_slots = NBmax - 1: slot s of request r holds logical block s for every
+    candidate block s < n_cand_r (slot_map = s, later slots free: -1), and slot k_slots holds the
+    request's local block nb_r - 1, as the sparse pools do. Only page copies happen here (torch
+    indexing, host to device); pool_v is transposed per head as the attention kernel reads it.
+    """
+    import numpy as np
+    host_k, host_v = host_k.view(torch.bfloat16), host_v.view(torch.bfloat16)  # bf16 bits in any 16-bit dtype
+    bt = np.asarray(block_table)
+    lens = np.asarray(ctx_len)
+    R, NB = bt.shape
+    _, H, B, D = host_k.shape
+    ks = NB - 1
+    pool_k = torch.zeros((R, NB, H, B, D), dtype=torch.bfloat16, device=device)
+    pool_v = torch.zeros((R, NB, H, D, B), dtype=torch.bfloat16, device=device)
+    smap = torch.full((R, H, max(ks, 1)), -1, dtype=torch.int32)
+    for r in range(R):
+        L_r = max(0, min(int(lens[r]), NB * B))
+        nb = (L_r + B - 1) // B
+        n_cand = max(nb - 1, 0)
+        if n_cand:
+            pages = torch.from_numpy(bt[r, :n_cand].astype(np.int64))
+            pool_k[r, :n_cand].copy_(host_k[pages].to(device))
+            pool_v[r, :n_cand].copy_(host_v[pages].to(device).transpose(-1, -2))
+            smap[r, :, :n_cand] = torch.arange(n_cand, dtype=torch.int32)
+        if nb:
+            page = int(bt[r, nb - 1])
+            pool_k[r, ks].copy_(host_k[page].to(device))
+            pool_v[r, ks].copy_(host_v[page].to(device).transpose(-1, -2))
+    return pool_k, pool_v, smap.to(device), ks
+
+
 class KernelTimer:
     """HIP events around library calls, recorded on the stream each call runs on."""
 

@@ -11,7 +11,7 @@ import pytest
 import torch
 
 from oracle import oasis_oracle as O
-from paper_2608_08097_amd.path import DecodePath, LayerState
+from paper_2608_08097_amd.path import DecodePath, LayerState, dense_working_set
 import paper_2608_08097_amd as P
 from tests.gpu_util import (assert_attn_close, assert_lse_close, assert_scores_close, as_np_bits, dev_bf16,
                             dev_i32, host_bits, note, pinned_pages, selection_diff)
@@ -55,11 +55,14 @@ def _oracle_request(w, hk, hv, r, ctx, q, K):
     return dict(s=s, sel=sel, cnt=cnt, smap=smap, moved=moved, out=out, lse=lse)
 
 
-@pytest.mark.parametrize("name", ["c1", "c2", "c4", "c5"])
-def test_fullsize_serial_step(name):
+@pytest.mark.parametrize("name,budget", [("c1", None), ("c2", None), ("c4", 1024), ("c4", 2048), ("c4", 4096),
+                                         ("c5", None)])
+def test_fullsize_serial_step(name, budget):
+    """One serial step of each configuration; c4 at each budget of its sweep (1,024 / 2,048 / 4,096 tokens:
+    K = 64 / 128 / 256 blocks, §5.2: the budget is the sparsification threshold)."""
     w, hk_t, hv_t = _tier(name, ar_queries=True)
     c = w.cfg
-    K = c.K
+    K = c.K if budget is None else budget // c.block_size
     d = _dims(w)
     ctx = w.ctx_len(0)
     q = w.queries(0)
@@ -81,6 +84,35 @@ def test_fullsize_serial_step(name):
         assert np.array_equal(smap[r:r + 1], ref["smap"]) and np.array_equal(moved[r:r + 1], ref["moved"])
         assert_attn_close(out[r:r + 1], ref["out"], f"{name} request {r}")
         assert_lse_close(lse[r:r + 1], ref["lse"])
+
+
+def test_fullsize_dense_c4():
+    """The benchmark's dense comparison exactly as bench.py runs it: 8 x 131,072 tokens resident in HBM, every
+    block in the slot of its own id, k_slots = 8,191 (4,096 units of 32 tokens per KV head, about 256 per
+    wave, so the lazily rescaled online softmax runs its longest loop), against the oracle's dense
+    attention over the paged host tier for sampled (request, KV head) pairs."""
+    w, hk_t, hv_t = _tier("c4", ar_queries=True)
+    c = w.cfg
+    d = _dims(w)
+    G = c.G
+    ctx = w.ctx_len(0)
+    q = w.queries(0)
+    pool_k, pool_v, smap, ks = dense_working_set(hk_t, hv_t, w.block_table, ctx)
+    assert ks == w.NBmax - 1 == 8191
+    out = torch.empty((c.num_reqs, c.T, c.num_q_heads, c.head_dim), dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((c.num_reqs, c.T, c.num_q_heads), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(P.oasis_attn_workspace_bytes(d, c.T, ks), dtype=torch.uint8, device="cuda")
+    note(f"full-size dense c4: R={c.num_reqs} L={int(ctx[0])} k_slots={ks}")
+    P.oasis_sparse_decode_attn(d, dev_bf16(q), c.T, pool_k, pool_v, smap, ks, dev_i32(ctx), None, out, lse, ws)
+    torch.cuda.synchronize()
+    out_np, lse_np = host_bits(out), lse.cpu().numpy()
+    del pool_k, pool_v
+    hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
+    for r, h in [(0, 0), (3, 5), (7, 7)]:
+        ref_o, ref_l = O.dense_attend(q[r:r + 1, :, h * G:(h + 1) * G], hk[:, h:h + 1], hv[:, h:h + 1],
+                                      w.block_table[r:r + 1], ctx[r:r + 1], c.block_size)
+        assert_attn_close(out_np[r:r + 1, :, h * G:(h + 1) * G], ref_o, f"dense c4 request {r} KV head {h}")
+        assert_lse_close(lse_np[r:r + 1, :, h * G:(h + 1) * G], ref_l)
 
 
 def test_fullsize_pipelined_capped_c4():

@@ -79,7 +79,7 @@
 extern "C" {
 #endif
 
-#define OASIS_ABI_VERSION 5
+#define OASIS_ABI_VERSION 6
 
 /* Only the entry points below are exported from liboasis.so. */
 #if defined(__GNUC__) || defined(__clang__)
@@ -258,8 +258,11 @@ OASIS_API oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t
 OASIS_API oasis_status oasis_union_selection(const oasis_dims* dims, const int32_t* sel, const int32_t* sel_count,
                                    int32_t k, int32_t* union_ids, int32_t* union_count, void* stream);
 
-/* Bytes of workspace oasis_sparse_decode_attn needs for these sizes (0 if invalid).
- * Calls that run at the same time need separate workspaces. */
+/* Bytes of workspace oasis_sparse_decode_attn needs for these sizes: the split
+ * partials (fp32 output, maximum and sum per split and row), 0 when a single
+ * split per (request, KV head) suffices (then the workspace may be NULL) or
+ * when the sizes are invalid. Calls that run at the same time need separate
+ * workspaces. */
 OASIS_API size_t oasis_attn_workspace_bytes(const oasis_dims* dims, int32_t num_q_tokens, int32_t k_slots);
 
 /*

@@ -59,7 +59,7 @@ def dims(num_reqs, num_q_heads, num_kv_heads, head_dim, block_size, max_blocks) 
 
 
 _lib = None
-ABI_VERSION = 5  # OASIS_ABI_VERSION of include/oasis.h
+ABI_VERSION = 6  # OASIS_ABI_VERSION of include/oasis.h
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -314,8 +314,9 @@ def oasis_sparse_decode_attn(d: OasisDims, q, num_q_tokens: int, pool_k, pool_v,
         ctypes.byref(d), _dev(q, "q", _BF16), int(num_q_tokens), _dev(pool_k, "pool_k", _BF16),
         _dev(pool_v, "pool_v", _BF16), _dev(slot_map, "slot_map", _I32T, nullable=k_slots == 0), int(k_slots),
         _dev(ctx_len, "ctx_len", _I32T), float(scale), _dev(out, "out", _BF16),
-        _dev(lse, "lse", _F32, nullable=True), _dev(workspace, "workspace", (torch.uint8,)),
-        int(workspace.numel()), _stream(stream)))
+        _dev(lse, "lse", _F32, nullable=True),
+        _dev(workspace, "workspace", (torch.uint8,), nullable=workspace is None or workspace.numel() == 0),
+        int(workspace.numel()) if workspace is not None else 0, _stream(stream)))
 
 
 # --- native step issuer --------------------------------------------------------

@@ -197,7 +197,7 @@ oasis_status make_attn_args(const oasis_dims* dims, const uint16_t* q, int32_t n
   if (k_slots > 0) REQUIRE_PTR(slot_map, fn);
   const AttnPlan p = attn_plan(dims->num_reqs, dims->num_q_heads, dims->num_kv_heads, num_q_tokens,
                                dims->block_size, k_slots);
-  if (!workspace || workspace_bytes < p.bytes)
+  if (p.bytes > 0 && (!workspace || workspace_bytes < p.bytes))
     return fail(OASIS_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", fn, workspace_bytes, p.bytes);
   AttnArgs t{};
   t.q = q;

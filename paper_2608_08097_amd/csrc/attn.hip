@@ -550,8 +550,9 @@ AttnPlan attn_plan(int R, int Hq, int Hkv, int T, int B, int k_slots) {
   if (want < 1) want = 1;
   p.units_per_split = (int)((p.n_units + want - 1) / want);
   p.nsplit = (p.n_units + p.units_per_split - 1) / p.units_per_split;
-  p.part_o_floats = (size_t)nrh * p.nsplit * p.rows * kHeadDim;
-  p.part_ml_floats = (size_t)nrh * p.nsplit * p.rows * 2;
+  // partials exist only with several splits (one split writes the outputs itself)
+  p.part_o_floats = p.nsplit > 1 ? (size_t)nrh * p.nsplit * p.rows * kHeadDim : 0;
+  p.part_ml_floats = p.nsplit > 1 ? (size_t)nrh * p.nsplit * p.rows * 2 : 0;
   p.bytes = (p.part_o_floats + p.part_ml_floats) * sizeof(float);
   return p;
 }

@@ -48,7 +48,7 @@ def test_exports_match_header(lib):
 
 
 def test_abi_version(lib):
-    assert lib.oasis_abi_version() == 5
+    assert lib.oasis_abi_version() == 6
 
 
 def test_argument_checks_without_gpu(lib):
@@ -126,8 +126,11 @@ def test_pipeline_argument_checks_without_gpu(lib):
 def test_workspace_sizes(lib):
     d = lib.dims(8, 32, 8, 128, 16, 8192)
     ws = lib.oasis_attn_workspace_bytes(d, 5, 128)
-    assert ws > 0 and ws % 4 == 0
+    # 64 (request, KV head) pairs x 4 splits x 20 rows x (128 outputs + max + sum) floats
+    assert ws == 64 * 4 * 20 * 130 * 4
     assert lib.oasis_attn_workspace_bytes(lib.dims(1, 32, 8, 64, 16, 1), 5, 4) == 0
+    # 512 pairs fill the chip with one split each: no partials, no workspace
+    assert lib.oasis_attn_workspace_bytes(lib.dims(64, 32, 8, 128, 16, 1024), 5, 128) == 0
 
 
 def test_local_block_pages_cover_every_local_block():

@@ -706,16 +706,24 @@ def test_pipeline_abi_errors_on_device():
 
 def test_abi_errors_on_device():
     d = P.dims(1, 32, 8, 128, 16, 16)
-    T, k = 5, 4
+    T, k = 5, 128                       # 8 pairs over 16 splits: partials need a workspace
     q = torch.zeros((1, T, 32, 128), dtype=torch.bfloat16, device="cuda")
     pool = torch.zeros((1, k + 1, 8, 16, 128), dtype=torch.bfloat16, device="cuda")
     smap = torch.full((1, 8, k), -1, dtype=torch.int32, device="cuda")
     ctx = torch.ones(1, dtype=torch.int32, device="cuda")
     out = torch.zeros((1, T, 32, 128), dtype=torch.bfloat16, device="cuda")
     small = torch.empty(8, dtype=torch.uint8, device="cuda")
+    assert P.oasis_attn_workspace_bytes(d, T, k) > 8
     with pytest.raises(P.OasisError) as e:
         P.oasis_sparse_decode_attn(d, q, T, pool, pool, smap, k, ctx, None, out, None, small)
     assert e.value.status == 4
+    # a single split per pair needs no workspace: an empty one is accepted
+    k1 = 4
+    assert P.oasis_attn_workspace_bytes(d, T, k1) == 0
+    P.oasis_sparse_decode_attn(d, q, T, pool[:, :k1 + 1].contiguous(), pool[:, :k1 + 1].contiguous(),
+                               smap[:, :, :k1].contiguous(), k1, ctx, None, out, None,
+                               torch.empty(0, dtype=torch.uint8, device="cuda"))
+    torch.cuda.synchronize()
     host = torch.zeros((4, 8, 16, 128), dtype=torch.bfloat16)  # not pinned
     with pytest.raises(ValueError):
         P.oasis_build_summaries(d, host, torch.zeros((1, 16), dtype=torch.int32, device="cuda"), ctx,

@@ -286,6 +286,29 @@ OASIS_API oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const ui
                                       void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * oasis_sparse_decode_attn without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving loops
+ * that must not call the allocator, harnesses that forbid it). Same operation,
+ * arguments, layouts and checks as oasis_sparse_decode_attn; the split partials
+ * go to a scratch array of the library in device memory: OASIS_NOALLOC_SCRATCH_BYTES
+ * (32 MiB) per GPU, held from the library's load until the process ends. Sizes
+ * whose oasis_attn_workspace_bytes exceeds it return OASIS_ERR_UNSUPPORTED
+ * without launching. Nothing is allocated, on the host or the device; the first
+ * call on a device looks up the scratch array's address there (one runtime
+ * query, not an allocation). Every call on one GPU shares that GPU's scratch:
+ * calls that overlap in time on one GPU (different streams, or a graph replayed
+ * beside another call) race and may corrupt each other's results; order them on
+ * one stream. The scratch needs no clearing between calls (each call writes the
+ * partials it reads).
+ */
+#define OASIS_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+OASIS_API oasis_status oasis_sparse_decode_attn_noalloc(const oasis_dims* dims, const uint16_t* q,
+                                              int32_t num_q_tokens, const uint16_t* pool_k,
+                                              const uint16_t* pool_v, const int32_t* slot_map, int32_t k_slots,
+                                              const int32_t* ctx_len, float scale, uint16_t* out, float* lse,
+                                              void* stream);
+
+/*
  * Native step issuer for the layer-pipelined schedule (paper §4.2.2, the
  * asynchronous prefetch pipeline figure and Eq. "prefetch-rate"; §5.1: the
  * stages run on background streams and events order each layer's chain).

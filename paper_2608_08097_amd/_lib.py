@@ -24,7 +24,8 @@ EXPORTS = (
     "oasis_last_error", "oasis_abi_version", "oasis_build_summaries", "oasis_update_summaries",
     "oasis_copy_blocks", "oasis_score_blocks",
     "oasis_select_topk", "oasis_stage_blocks",
-    "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn", "oasis_union_selection",
+    "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn", "oasis_sparse_decode_attn_noalloc",
+    "oasis_union_selection",
     "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_set_local_source",
     "oasis_pipeline_set_plan_stream", "oasis_pipeline_step",
     "oasis_pipeline_join",
@@ -103,6 +104,9 @@ def lib() -> ctypes.CDLL:
         L.oasis_sparse_decode_attn.restype = _I32
         L.oasis_sparse_decode_attn.argtypes = [_DIMS, _P, _I32, _P, _P, _P, _I32, _P, ctypes.c_float, _P, _P,
                                                _P, _SZ, _P]
+        L.oasis_sparse_decode_attn_noalloc.restype = _I32
+        L.oasis_sparse_decode_attn_noalloc.argtypes = [_DIMS, _P, _I32, _P, _P, _P, _I32, _P, ctypes.c_float, _P,
+                                                       _P, _P]
         L.oasis_pipeline_create.restype = _I32
         L.oasis_pipeline_create.argtypes = [_DIMS, _I32, _I32, _I32, _I32, _I32, ctypes.c_float, _P, _P, _I64, _P,
                                             _I32, _P, _P, ctypes.POINTER(_P)]
@@ -317,6 +321,29 @@ def oasis_sparse_decode_attn(d: OasisDims, q, num_q_tokens: int, pool_k, pool_v,
         _dev(lse, "lse", _F32, nullable=True),
         _dev(workspace, "workspace", (torch.uint8,), nullable=workspace is None or workspace.numel() == 0),
         int(workspace.numel()) if workspace is not None else 0, _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20  # OASIS_NOALLOC_SCRATCH_BYTES of include/oasis.h
+
+
+def oasis_sparse_decode_attn_noalloc(d: OasisDims, q, num_q_tokens: int, pool_k, pool_v, slot_map, k_slots: int,
+                                     ctx_len, scale: float | None, out, lse, stream=None) -> None:
+    """oasis_sparse_decode_attn with the library's own scratch instead of a workspace (allocates nothing)."""
+    if scale is None:
+        scale = 1.0 / math.sqrt(d.head_dim)
+    R, H, B, D = d.num_reqs, d.num_kv_heads, d.block_size, d.head_dim
+    _need(q, R * num_q_tokens * d.num_q_heads * D, "q")
+    _need(out, R * num_q_tokens * d.num_q_heads * D, "out")
+    _need(lse, R * num_q_tokens * d.num_q_heads, "lse")
+    _need(pool_k, R * (k_slots + 1) * H * B * D, "pool_k")
+    _need(pool_v, R * (k_slots + 1) * H * B * D, "pool_v")
+    _need(slot_map, R * H * k_slots, "slot_map")
+    _need(ctx_len, R, "ctx_len")
+    _check("oasis_sparse_decode_attn_noalloc", lib().oasis_sparse_decode_attn_noalloc(
+        ctypes.byref(d), _dev(q, "q", _BF16), int(num_q_tokens), _dev(pool_k, "pool_k", _BF16),
+        _dev(pool_v, "pool_v", _BF16), _dev(slot_map, "slot_map", _I32T, nullable=k_slots == 0), int(k_slots),
+        _dev(ctx_len, "ctx_len", _I32T), float(scale), _dev(out, "out", _BF16),
+        _dev(lse, "lse", _F32, nullable=True), _stream(stream)))
 
 
 # --- native step issuer --------------------------------------------------------

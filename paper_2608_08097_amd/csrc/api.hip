@@ -409,4 +409,36 @@ oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const uint16_t* q,
   return hip_status(oasis::launch_attn(a, static_cast<hipStream_t>(stream)), fn);
 }
 
+oasis_status oasis_sparse_decode_attn_noalloc(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens,
+                                              const uint16_t* pool_k, const uint16_t* pool_v,
+                                              const int32_t* slot_map, int32_t k_slots, const int32_t* ctx_len,
+                                              float scale, uint16_t* out, float* lse, void* stream) {
+  static const char* fn = "oasis_sparse_decode_attn_noalloc";
+  oasis_status st = oasis::check_dims(dims, fn);
+  if (st != OASIS_OK) return st;
+  if (num_q_tokens < 1) return fail(OASIS_ERR_INVALID_ARG, "%s: num_q_tokens < 1", fn);
+  if (k_slots < 0) return fail(OASIS_ERR_INVALID_ARG, "%s: k_slots < 0", fn);
+  const size_t need = oasis::attn_plan(dims->num_reqs, dims->num_q_heads, dims->num_kv_heads, num_q_tokens,
+                                       dims->block_size, k_slots)
+                          .bytes;
+  if (need > oasis::kNoAllocScratchBytes)
+    return fail(OASIS_ERR_UNSUPPORTED, "%s: these sizes need %zu bytes of scratch, more than the %zu it holds", fn,
+                need, oasis::kNoAllocScratchBytes);
+  // every argument is checked before the first runtime call (the scratch
+  // address is not needed for that), then the arguments are built on it
+  oasis::AttnArgs a{};
+  static int sentinel;
+  st = oasis::make_attn_args(dims, q, num_q_tokens, pool_k, pool_v, slot_map, k_slots, ctx_len, scale, out, lse,
+                             &sentinel, oasis::kNoAllocScratchBytes, &a, fn);
+  if (st != OASIS_OK) return st;
+  if (dims->num_reqs == 0) return ok();
+  void* scratch = nullptr;
+  const hipError_t e = oasis::noalloc_scratch(&scratch);
+  if (e != hipSuccess) return hip_status(e, fn);
+  st = oasis::make_attn_args(dims, q, num_q_tokens, pool_k, pool_v, slot_map, k_slots, ctx_len, scale, out, lse,
+                             scratch, oasis::kNoAllocScratchBytes, &a, fn);
+  if (st != OASIS_OK) return st;
+  return hip_status(oasis::launch_attn(a, static_cast<hipStream_t>(stream)), fn);
+}
+
 }  // extern "C"

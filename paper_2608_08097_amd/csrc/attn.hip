@@ -29,6 +29,8 @@
 // So K and V go straight from HBM into MFMA registers with 16-byte loads and
 // no LDS round trip; every lane owns one query row, so the running max and sum
 // need only two cross-lane exchanges per unit.
+#include <mutex>
+
 #include "oasis_internal.h"
 
 namespace oasis {
@@ -559,6 +561,36 @@ AttnPlan attn_plan(int R, int Hq, int Hkv, int T, int B, int k_slots) {
 
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s, const LaunchTiming& t) {
   return a.B == 16 ? launch_bs<16>(a, s, t) : launch_bs<32>(a, s, t);
+}
+
+// Scratch of the allocation-free attention entry point: the split partials, in
+// a file-scope device array that every GPU the library runs on holds from
+// module load until the process ends (kNoAllocScratchBytes each). Host code
+// never passes the array's name to a kernel: that is a host-side stand-in, not
+// a device address. Its address on each device comes from hipGetSymbolAddress,
+// taken once per device with that device current, and only that address is
+// handed to the kernels.
+namespace {
+__device__ __align__(256) float scratch[kNoAllocScratchBytes / sizeof(float)];
+constexpr int kMaxDevices = 64;
+void* g_scratch_ptr[kMaxDevices] = {};
+std::mutex g_scratch_mu;
+}  // namespace
+
+hipError_t noalloc_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace oasis

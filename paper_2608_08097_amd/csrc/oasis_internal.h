@@ -198,6 +198,10 @@ struct AttnPlan {
 };
 AttnPlan attn_plan(int R, int Hq, int Hkv, int T, int B, int k_slots);
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s, const LaunchTiming& t = {});
+// Scratch of oasis_sparse_decode_attn_noalloc: a device array of this many bytes
+// per GPU (attn.hip); noalloc_scratch returns its address on the current device.
+constexpr size_t kNoAllocScratchBytes = OASIS_NOALLOC_SCRATCH_BYTES;
+hipError_t noalloc_scratch(void** ptr);
 
 // --- argument checks shared by the entry points (api.hip) ---------------------
 // Each builder validates like the entry point of the same operation (fn names

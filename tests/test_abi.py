@@ -133,6 +133,28 @@ def test_workspace_sizes(lib):
     assert lib.oasis_attn_workspace_bytes(lib.dims(64, 32, 8, 128, 16, 1024), 5, 128) == 0
 
 
+def test_noalloc_attention_checks_without_gpu(lib):
+    """The allocation-free attention entry point checks like the workspace form and rejects sizes whose
+    partials exceed its scratch, all before any HIP call."""
+    L = lib.lib()
+    bad_hd = lib.dims(1, 32, 8, 64, 16, 512)
+    assert L.oasis_sparse_decode_attn_noalloc(ctypes.byref(bad_hd), None, 5, None, None, None, 128, None, 0.1,
+                                              None, None, None) == 2
+    ok = lib.dims(8, 32, 8, 128, 16, 8192)
+    assert L.oasis_sparse_decode_attn_noalloc(ctypes.byref(ok), None, 0, None, None, None, 128, None, 0.1, None,
+                                              None, None) == 1
+    assert L.oasis_sparse_decode_attn_noalloc(ctypes.byref(ok), None, 5, None, None, None, 128, None, 0.1, None,
+                                              None, None) == 1
+    assert "is NULL" in lib.oasis_last_error()
+    # 504 pairs x 2 splits x 80 rows x 130 floats = 41.9 MB of partials > the 32 MiB scratch
+    big = lib.dims(63, 128, 8, 128, 16, 8192)
+    need = lib.oasis_attn_workspace_bytes(big, 5, 128)
+    assert need == 504 * 2 * 80 * 130 * 4 and need > lib._lib.NOALLOC_SCRATCH_BYTES
+    assert L.oasis_sparse_decode_attn_noalloc(ctypes.byref(big), None, 5, None, None, None, 128, None, 0.1, None,
+                                              None, None) == 2
+    assert "scratch" in lib.oasis_last_error()
+
+
 def test_local_block_pages_cover_every_local_block():
     """The device copy of the active blocks holds, for every request and step, the block that is
     local at that step, at the index its table gives."""

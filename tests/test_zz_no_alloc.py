@@ -1,0 +1,61 @@
+"""The allocation-free attention entry point (library scratch instead of a workspace) against the
+workspace entry point, through the C ABI: two calls in a row, the second with smaller sizes, then the
+first again. Same kernels, so the outputs must be bit-identical; they are also checked against the
+oracle at the attention tolerance."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_08097_amd as P
+from oracle import oasis_oracle as O
+from tests.gpu_util import (assert_attn_close, assert_lse_close, dev_bf16, dev_i32, host_bits, note,
+                            pool_v_from_htd)
+from workloads import random_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(seed, R, Hq, Hkv, T, B, ks, lens, free=0.2):
+    q = random_bf16(900 + seed, (R, T, Hq, 128))
+    pk = random_bf16(910 + seed, (R, ks + 1, Hkv, B, 128))
+    pv = random_bf16(920 + seed, (R, ks + 1, Hkv, B, 128))
+    rng = np.random.default_rng(930 + seed)
+    smap = np.where(rng.random((R, Hkv, ks)) < free, -1, rng.integers(0, 10 ** 6, (R, Hkv, ks))).astype(np.int32)
+    ctx = np.array(lens, np.int32)
+    return q, pk, pv, smap, ctx
+
+
+def _both(q, pk, pv, smap, ctx, R, Hq, Hkv, T, B, ks):
+    d = P.dims(R, Hq, Hkv, 128, B, max(1, (int(ctx.max()) + B - 1) // B))
+    need = P.oasis_attn_workspace_bytes(d, T, ks)
+    assert 0 < need <= P._lib.NOALLOC_SCRATCH_BYTES, need   # several splits: the scratch is used
+    args = (dev_bf16(q), T, dev_bf16(pk), dev_bf16(pool_v_from_htd(pv)), dev_i32(smap), ks, dev_i32(ctx), None)
+    out_w = torch.zeros((R, T, Hq, 128), dtype=torch.bfloat16, device="cuda")
+    lse_w = torch.zeros((R, T, Hq), dtype=torch.float32, device="cuda")
+    out_n = torch.full_like(out_w, float("nan"))
+    lse_n = torch.full_like(lse_w, float("nan"))
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    P.oasis_sparse_decode_attn(d, *args, out_w, lse_w, ws)
+    P.oasis_sparse_decode_attn_noalloc(d, *args, out_n, lse_n)
+    torch.cuda.synchronize()
+    return host_bits(out_w), lse_w.cpu().numpy(), host_bits(out_n), lse_n.cpu().numpy()
+
+
+def test_noalloc_matches_workspace_entry_point():
+    big = dict(R=8, Hq=32, Hkv=8, T=5, B=16, ks=128)                 # 64 pairs x 4 splits x 20 rows
+    small = dict(R=2, Hq=16, Hkv=8, T=3, B=32, ks=32)                # 16 pairs x 9 splits x 6 rows
+    cases = [(1, big, [2064, 1800, 2050, 33, 2064, 1999, 2048, 2063]), (2, small, [1040, 600])]
+    first = None
+    for seed, sz, lens in cases + [cases[0]]:
+        q, pk, pv, smap, ctx = _inputs(seed, lens=lens, **sz)
+        note(f"noalloc attention seed={seed} {sz}")
+        ow, lw, on, ln = _both(q, pk, pv, smap, ctx, **sz)
+        assert np.array_equal(on, ow), "outputs differ from the workspace entry point"
+        assert np.array_equal(ln, lw), "log-sum-exp differs from the workspace entry point"
+        ref_o, ref_l = O.sparse_attend(q, pk, pv, smap, ctx, sz["B"])
+        assert_attn_close(on, ref_o, f"noalloc seed {seed}")
+        assert_lse_close(ln, ref_l)
+        if first is None:
+            first = on
+        elif seed == cases[0][0]:
+            assert np.array_equal(on, first), "the repeated first call differs"

@@ -85,6 +85,9 @@ def parse():
                     help="per-step fetch cap as a fraction of K (paper default 0.05); >= 1 admits every miss")
     ap.add_argument("--plan-stream", choices=("auto", "transfer", "prediction"), default="auto",
                     help="stream that plans each step's transfer (auto: prediction for c3, transfer otherwise)")
+    ap.add_argument("--fused-prediction", choices=("auto", "off", "on"), default="auto",
+                    help="score and select (and plan) in one kernel per step: auto = with >= 256 (request, KV head) "
+                         "pairs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention comparison")
@@ -106,6 +109,12 @@ def plan_on_prediction(args) -> bool:
     if args.plan_stream == "auto":
         return args.workload == "c3"
     return args.plan_stream == "prediction"
+
+
+def fused_mode(args) -> int:
+    from paper_2608_08097_amd import _lib as L
+    return {"auto": L.FUSED_PREDICTION_AUTO, "off": L.FUSED_PREDICTION_OFF,
+            "on": L.FUSED_PREDICTION_ON}[args.fused_prediction]
 
 
 def log(msg):
@@ -346,7 +355,8 @@ def main():
     ctx_d = torch.from_numpy(ctx).cuda()
     fetch_cap = K if args.fetch_ratio >= 1.0 else max(1, int(math.floor(args.fetch_ratio * K)))
     path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=fetch_cap,
-                      plan_on_prediction=plan_on_prediction(args))
+                      plan_on_prediction=plan_on_prediction(args),
+                      fused_prediction=fused_mode(args))
     layers = [path.new_layer() for _ in range(NL)]
     path.build_summaries(layers[0], ctx_d)
     for st in layers[1:]:
@@ -451,6 +461,7 @@ def main():
             "global_batch": c.num_reqs, "seq_len": int(ctx.max()), "budget": args.budget,
             "fetch_ratio": args.fetch_ratio if fetch_cap < K else "all", "fetch_cap": fetch_cap,
             "parallelism": "single GPU", "plan_stream": "prediction" if plan_on_prediction(args) else "transfer",
+            "fused_prediction": args.fused_prediction,
         },
         "roofline": {
             "bound": "hbm", "kernel": "score_kernel (oasis_score_blocks)",
@@ -519,7 +530,8 @@ def run_reasoning(args, P, torch, DecodePath):
     bt = torch.from_numpy(w.block_table).cuda()
     ctx_d = [torch.from_numpy(w.ctx_len(s_)).cuda() for s_ in range(S)]
     path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=fetch_cap,
-                      max_layers=NL, plan_on_prediction=plan_on_prediction(args))
+                      max_layers=NL, plan_on_prediction=plan_on_prediction(args),
+                      fused_prediction=fused_mode(args))
     # The blocks that are a request's local block during the run live in device
     # pages, as a model writes its newest tokens on the GPU: the local refresh
     # and the compressed-key update of a completed block read them there, and
@@ -593,7 +605,8 @@ def run_reasoning(args, P, torch, DecodePath):
                                f"U[4,096, 16,384] generated tokens, block 16, {c.num_draft} draft tokens, budget "
                                f"{args.budget} (K={K}), fetch cap {fetch_cap}, {S} steps of one token",
                    "global_batch": c.num_reqs, "layers": NL, "fetch_cap": fetch_cap,
-                   "plan_stream": "prediction" if plan_on_prediction(args) else "transfer"},
+                   "plan_stream": "prediction" if plan_on_prediction(args) else "transfer",
+                   "fused_prediction": args.fused_prediction},
         "tokens_per_s": round(c.num_reqs * S / elapsed, 1),
         "decode_step_ms_all_layers": round(t_step_us / 1e3, 3),
         "prefetch_rate": {"delta_prefetch_us": round(delta, 2), "t_pred_us": round(prof["score"] + prof["topk"], 2),

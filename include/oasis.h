@@ -198,6 +198,23 @@ OASIS_API oasis_status oasis_select_topk(const oasis_dims* dims, const float* sc
                                int32_t k, int32_t* sel, int32_t* sel_count, void* stream);
 
 /*
+ * oasis_score_blocks followed by oasis_select_topk in one kernel: one workgroup
+ * per (request, KV head) scores the head's candidate blocks and selects its
+ * top k from them (paper §4.2.1-§4.2.2), so the scores make no round trip
+ * between two launches. Results (scores, sel, sel_count) are bit-identical to
+ * the two calls. Worth it when the rows are many and short (hundreds of
+ * (request, KV head) pairs with a few thousand blocks each); with few long rows
+ * the two calls spread each row over many workgroups. Supported for
+ * 5 <= num_draft * G <= 32 scoring rows and max_blocks <= 16,384
+ * (OASIS_ERR_UNSUPPORTED otherwise); arguments as in the two calls. Device
+ * pointers.
+ */
+OASIS_API oasis_status oasis_score_select(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens,
+                                int32_t first_draft, int32_t num_draft, const uint16_t* kmax,
+                                const uint16_t* kmin, const int32_t* ctx_len, int32_t k, float* scores,
+                                int32_t* sel, int32_t* sel_count, void* stream);
+
+/*
  * Delta selection + KV transfer into the HBM working set (paper §4.2.3: resident
  * hits stay and move no bytes; non-selected residents are evicted least-recently-
  * selected first; each admitted miss is paired with one eviction target; §4.3:
@@ -320,7 +337,8 @@ OASIS_API oasis_status oasis_sparse_decode_attn_noalloc(const oasis_dims* dims, 
  *     working set;
  *   prediction stream: once q is ready and the layer's previous transfer has
  *     read sel and scores, oasis_score_blocks on the draft rows of q and
- *     oasis_select_topk (the prediction for the layer's next step);
+ *     oasis_select_topk (the prediction for the layer's next step; both in one
+ *     kernel under oasis_pipeline_set_fused_prediction);
  *   transfer stream: once the prediction is ready and this step's attention
  *     has read the pools, oasis_stage_blocks (delta selection with the fetch
  *     cap, then the gather; the paper's selection and transfer stages are one
@@ -412,6 +430,20 @@ OASIS_API oasis_status oasis_pipeline_set_local_source(oasis_pipeline* pipeline,
 #define OASIS_PLAN_ON_TRANSFER 0
 #define OASIS_PLAN_ON_PREDICTION 1
 OASIS_API oasis_status oasis_pipeline_set_plan_stream(oasis_pipeline* pipeline, int32_t where);
+
+/* How a step predicts (paper §4.2.1-§4.2.2). OASIS_FUSED_PREDICTION_AUTO (the
+ * default): scoring and top-K (and the plan, when it runs on the prediction
+ * stream) in one kernel with one workgroup per (request, KV head), as
+ * oasis_score_select does, when the step has at least 256 such pairs and
+ * oasis_score_select supports the sizes; otherwise the separate kernels.
+ * OASIS_FUSED_PREDICTION_OFF: always the separate kernels.
+ * OASIS_FUSED_PREDICTION_ON: the fused kernel whenever the sizes are supported.
+ * The results are the same either way. Takes effect from the next step.
+ * Errors: INVALID_ARG for a NULL pipeline or another value. */
+#define OASIS_FUSED_PREDICTION_AUTO 0
+#define OASIS_FUSED_PREDICTION_OFF 1
+#define OASIS_FUSED_PREDICTION_ON 2
+OASIS_API oasis_status oasis_pipeline_set_fused_prediction(oasis_pipeline* pipeline, int32_t mode);
 
 /* Issue one decode step of `layer` (see above). q: bf16 device [R][T][Hq][d];
  * ctx_len: device [R]; prev_ctx_len (nullable, device [R]): the lengths at the

@@ -22,12 +22,12 @@ STATUS = {0: "OASIS_OK", 1: "OASIS_ERR_INVALID_ARG", 2: "OASIS_ERR_UNSUPPORTED",
 
 EXPORTS = (
     "oasis_last_error", "oasis_abi_version", "oasis_build_summaries", "oasis_update_summaries",
-    "oasis_copy_blocks", "oasis_score_blocks",
+    "oasis_copy_blocks", "oasis_score_blocks", "oasis_score_select",
     "oasis_select_topk", "oasis_stage_blocks",
     "oasis_attn_workspace_bytes", "oasis_sparse_decode_attn", "oasis_sparse_decode_attn_noalloc",
     "oasis_union_selection",
     "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_set_local_source",
-    "oasis_pipeline_set_plan_stream", "oasis_pipeline_step",
+    "oasis_pipeline_set_plan_stream", "oasis_pipeline_set_fused_prediction", "oasis_pipeline_step",
     "oasis_pipeline_join",
     "oasis_pipeline_destroy", "oasis_pipeline_profile_begin", "oasis_pipeline_profile_end",
 )
@@ -97,6 +97,8 @@ def lib() -> ctypes.CDLL:
         L.oasis_stage_blocks.restype = _I32
         L.oasis_stage_blocks.argtypes = [_DIMS, _P, _P, _I64, _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _I32, _I32,
                                          _P, _P, _P, _P]
+        L.oasis_score_select.restype = _I32
+        L.oasis_score_select.argtypes = [_DIMS, _P, _I32, _I32, _I32, _P, _P, _P, _I32, _P, _P, _P, _P]
         L.oasis_union_selection.restype = _I32
         L.oasis_union_selection.argtypes = [_DIMS, _P, _P, _I32, _P, _P, _P]
         L.oasis_attn_workspace_bytes.restype = _SZ
@@ -110,6 +112,8 @@ def lib() -> ctypes.CDLL:
         L.oasis_pipeline_create.restype = _I32
         L.oasis_pipeline_create.argtypes = [_DIMS, _I32, _I32, _I32, _I32, _I32, ctypes.c_float, _P, _P, _I64, _P,
                                             _I32, _P, _P, ctypes.POINTER(_P)]
+        L.oasis_pipeline_set_fused_prediction.restype = _I32
+        L.oasis_pipeline_set_fused_prediction.argtypes = [_P, _I32]
         L.oasis_pipeline_set_layer.restype = _I32
         L.oasis_pipeline_set_layer.argtypes = [_P, _I32, ctypes.POINTER(OasisLayerBuffers)]
         L.oasis_pipeline_set_local_source.restype = _I32
@@ -261,6 +265,24 @@ def oasis_select_topk(d: OasisDims, scores, ctx_len, k: int, sel, sel_count, str
         _dev(sel, "sel", _I32T), _dev(sel_count, "sel_count", _I32T), _stream(stream)))
 
 
+def oasis_score_select(d: OasisDims, q, num_q_tokens: int, first_draft: int, num_draft: int, kmax, kmin, ctx_len,
+                       k: int, scores, sel, sel_count, stream=None) -> None:
+    """Scores and top-K in one kernel (the same results as oasis_score_blocks + oasis_select_topk)."""
+    R, H, NB, D = d.num_reqs, d.num_kv_heads, d.max_blocks, d.head_dim
+    _need(q, R * num_q_tokens * d.num_q_heads * D, "q")
+    _need(kmax, R * H * NB * D, "kmax")
+    _need(kmin, R * H * NB * D, "kmin")
+    _need(ctx_len, R, "ctx_len")
+    _need(scores, R * H * NB, "scores")
+    _need(sel, R * H * k, "sel")
+    _need(sel_count, R * H, "sel_count")
+    _check("oasis_score_select", lib().oasis_score_select(
+        ctypes.byref(d), _dev(q, "q", _BF16), int(num_q_tokens), int(first_draft), int(num_draft),
+        _dev(kmax, "kmax", _BF16), _dev(kmin, "kmin", _BF16), _dev(ctx_len, "ctx_len", _I32T), int(k),
+        _dev(scores, "scores", _F32), _dev(sel, "sel", _I32T), _dev(sel_count, "sel_count", _I32T),
+        _stream(stream)))
+
+
 def oasis_stage_blocks(d: OasisDims, host_k, host_v, host_block_table, ctx_len, sel, sel_count, scores, k: int,
                        slot_map, slot_stamp, step: int, fetch_cap: int, copy_local: bool, pool_k, pool_v,
                        moved, stream=None) -> None:
@@ -380,6 +402,16 @@ def oasis_pipeline_set_plan_stream(handle: int, where: int) -> None:
     """Plan each step's transfer on the transfer stream (PLAN_ON_TRANSFER) or in the top-K kernel
     on the prediction stream (PLAN_ON_PREDICTION)."""
     _check("oasis_pipeline_set_plan_stream", lib().oasis_pipeline_set_plan_stream(handle, int(where)))
+
+
+FUSED_PREDICTION_AUTO = 0  # OASIS_FUSED_PREDICTION_AUTO
+FUSED_PREDICTION_OFF = 1   # OASIS_FUSED_PREDICTION_OFF
+FUSED_PREDICTION_ON = 2    # OASIS_FUSED_PREDICTION_ON
+
+
+def oasis_pipeline_set_fused_prediction(handle: int, mode: int) -> None:
+    """Score and select (and plan) in one kernel per step: AUTO (many short rows), OFF or ON."""
+    _check("oasis_pipeline_set_fused_prediction", lib().oasis_pipeline_set_fused_prediction(handle, int(mode)))
 
 
 def oasis_pipeline_set_local_source(handle: int, d: OasisDims, k_pages, v_pages, block_table) -> None:

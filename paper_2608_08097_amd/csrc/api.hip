@@ -347,6 +347,27 @@ oasis_status oasis_select_topk(const oasis_dims* dims, const float* scores, cons
   return hip_status(oasis::launch_topk(a, static_cast<hipStream_t>(stream)), fn);
 }
 
+oasis_status oasis_score_select(const oasis_dims* dims, const uint16_t* q, int32_t num_q_tokens,
+                                int32_t first_draft, int32_t num_draft, const uint16_t* kmax,
+                                const uint16_t* kmin, const int32_t* ctx_len, int32_t k, float* scores,
+                                int32_t* sel, int32_t* sel_count, void* stream) {
+  static const char* fn = "oasis_score_select";
+  oasis::ScoreArgs sa{};
+  oasis::TopkArgs ta{};
+  oasis_status st =
+      oasis::make_score_args(dims, q, num_q_tokens, first_draft, num_draft, kmax, kmin, ctx_len, scores, &sa, fn);
+  if (st != OASIS_OK) return st;
+  if ((st = oasis::make_topk_args(dims, scores, ctx_len, k, sel, sel_count, &ta, fn)) != OASIS_OK) return st;
+  const int rows = num_draft * (dims->num_q_heads / dims->num_kv_heads);
+  if (rows <= oasis::kScoreValuMaxRows || rows > oasis::kScoreSelectMaxRows)
+    return fail(OASIS_ERR_UNSUPPORTED, "%s: %d scoring rows (%d to %d are supported)", fn, rows,
+                oasis::kScoreValuMaxRows + 1, oasis::kScoreSelectMaxRows);
+  if (dims->max_blocks > oasis::kScoreSelectMaxBlocks)
+    return fail(OASIS_ERR_UNSUPPORTED, "%s: max_blocks %d > %d", fn, dims->max_blocks, oasis::kScoreSelectMaxBlocks);
+  if (dims->num_reqs == 0) return ok();
+  return hip_status(oasis::launch_score_select(sa, ta, nullptr, static_cast<hipStream_t>(stream)), fn);
+}
+
 oasis_status oasis_stage_blocks(const oasis_dims* dims, const uint16_t* host_k, const uint16_t* host_v,
                                 int64_t num_pages, const int32_t* host_block_table, const int32_t* ctx_len,
                                 const int32_t* sel, const int32_t* sel_count, const float* scores, int32_t k,

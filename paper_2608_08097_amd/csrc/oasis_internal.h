@@ -177,6 +177,16 @@ inline size_t stage_ws_ints(long long nrh, int k) { return (size_t)nrh * (4 * (s
 // kernel; a.mode must be kStagePlanOnly (the plan goes to a.ws).
 hipError_t launch_topk_plan(const TopkArgs& t, const StageArgs& a, hipStream_t s, const LaunchTiming& lt = {});
 hipError_t launch_stage(const StageArgs& a, hipStream_t s, const LaunchTiming& t = {});
+// Scoring and top-K of each (request, KV head) in one workgroup (stage.hip), with
+// the transfer plan when `plan` is set (mode kStagePlanOnly, into plan->ws).
+// Scores and selections are identical to launch_score followed by launch_topk.
+// For 5 to kScoreSelectMaxRows scoring rows (more would not fit the registers of
+// a 1024-thread workgroup) and at most kScoreSelectMaxBlocks blocks per row.
+constexpr int kScoreSelectMaxRows = 32;
+constexpr int kScoreSelectMaxBlocks = 16384;
+bool score_select_supported(const ScoreArgs& sa);
+hipError_t launch_score_select(const ScoreArgs& sa, const TopkArgs& t, const StageArgs* plan, hipStream_t s,
+                               const LaunchTiming& lt = {});
 
 struct AttnArgs {
   const uint16_t* q;

@@ -23,6 +23,9 @@ constexpr int kFlagStride = 64;  // uint32 per counter (256 bytes)
 constexpr int kQ = 0, kPred = 1, kAttn = 2, kJoinPred = 3, kJoinXfer = 4, kStaged0 = 5;  // counter slots
 constexpr uint32_t kWrapGuard = 1u << 30;
 constexpr int kProfKinds = 4;  // attention (split + merge), scoring, top-K, staging
+// (request, KV head) pairs from which OASIS_FUSED_PREDICTION_AUTO scores and
+// selects in one kernel (one 1024-thread workgroup per pair: a full chip)
+constexpr long long kFusedMinPairs = 256;
 }  // namespace
 
 struct oasis_pipeline {
@@ -48,6 +51,7 @@ struct oasis_pipeline {
   bool* is_set;                 // [max_layers]
   int32_t** plan_ws;            // [max_layers]: device staging-plan workspace of each layer (set_layer)
   bool plan_on_pred;            // OASIS_PLAN_ON_PREDICTION
+  int32_t fused_pred;           // OASIS_FUSED_PREDICTION_*: score and top-K (+ plan) in one kernel
   // optional profile: timing events around each kernel of the next prof_cap steps
   int32_t prof_cap, prof_n;
   hipEvent_t* prof_ev;          // [prof_cap][kProfKinds][2]
@@ -299,6 +303,15 @@ oasis_status oasis_pipeline_set_plan_stream(oasis_pipeline* p, int32_t where) {
   return ok();
 }
 
+oasis_status oasis_pipeline_set_fused_prediction(oasis_pipeline* p, int32_t mode) {
+  static const char* fn = "oasis_pipeline_set_fused_prediction";
+  if (!p) return fail(OASIS_ERR_INVALID_ARG, "%s: pipeline is NULL", fn);
+  if (mode != OASIS_FUSED_PREDICTION_AUTO && mode != OASIS_FUSED_PREDICTION_OFF && mode != OASIS_FUSED_PREDICTION_ON)
+    return fail(OASIS_ERR_INVALID_ARG, "%s: mode = %d is not an OASIS_FUSED_PREDICTION_* value", fn, mode);
+  p->fused_pred = mode;
+  return ok();
+}
+
 oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_t* q, const int32_t* ctx_len,
                                  const int32_t* prev_ctx_len, int32_t max_new_blocks, int32_t step, int32_t growing,
                                  int32_t* moved, void* stream) {
@@ -367,11 +380,25 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   HIP_TRY(oasis::launch_attn(aa, fg, prof_timing(p, 0)), fn);
   HIP_TRY(signal_next(p, fg, kAttn, &cnt[kAttn]), fn);
   if (prev_ctx_len) HIP_TRY(oasis::launch_summaries(ua, p->pred), fn);
-  HIP_TRY(oasis::launch_score(sa, p->pred, prof_timing(p, 1)), fn);
-  if (p->plan_on_pred)
-    HIP_TRY(oasis::launch_topk_plan(ta, gp, p->pred, prof_timing(p, 2)), fn);
-  else
-    HIP_TRY(oasis::launch_topk(ta, p->pred, prof_timing(p, 2)), fn);
+  // one workgroup per (request, KV head) scores and selects (and plans) when
+  // the rows are many and short enough to fill the chip that way
+  const bool fused = oasis::score_select_supported(sa) &&
+                     (p->fused_pred == OASIS_FUSED_PREDICTION_ON ||
+                      (p->fused_pred == OASIS_FUSED_PREDICTION_AUTO &&
+                       (long long)d->num_reqs * d->num_kv_heads >= kFusedMinPairs));
+  if (fused) {
+    // profiled as scoring; the top-K span is left empty
+    HIP_TRY(oasis::launch_score_select(sa, ta, p->plan_on_pred ? &gp : nullptr, p->pred, prof_timing(p, 1)), fn);
+    const oasis::LaunchTiming tk = prof_timing(p, 2);
+    if (tk.start) HIP_TRY(hipEventRecord(tk.start, p->pred), fn);
+    if (tk.stop) HIP_TRY(hipEventRecord(tk.stop, p->pred), fn);
+  } else {
+    HIP_TRY(oasis::launch_score(sa, p->pred, prof_timing(p, 1)), fn);
+    if (p->plan_on_pred)
+      HIP_TRY(oasis::launch_topk_plan(ta, gp, p->pred, prof_timing(p, 2)), fn);
+    else
+      HIP_TRY(oasis::launch_topk(ta, p->pred, prof_timing(p, 2)), fn);
+  }
   HIP_TRY(signal_next(p, p->pred, kPred, &cnt[kPred]), fn);
   HIP_TRY(wait_for(p, p->xfer, kPred, cnt[kPred]), fn);
   HIP_TRY(wait_for(p, p->xfer, kAttn, cnt[kAttn]), fn);  // the gather overwrites slots the attention reads

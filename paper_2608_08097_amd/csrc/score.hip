@@ -2,13 +2,10 @@
 // of every candidate block for every draft row, maximum over the G x D rows of
 // a KV head.
 //
-// For one row q and a block with per-coordinate bounds kmin <= kmax,
-//   sum_d max(q_d kmin_d, q_d kmax_d) = sum_d (q+_d kmax_d + q-_d kmin_d)
-// with q+ = max(q, 0), q- = min(q, 0): exactly a dot product of [q+ | q-]
-// (2d bf16 values, exact) with [kmax ; kmin]. The rows of one KV head (5 to
-// 64 here; fewer go to the vector-ALU scorer of score_valu.hip) times a tile
-// of 16 blocks is therefore a dense [rows x 256] x [256 x 16] product, done
-// with v_mfma_f32_16x16x32_bf16 (fp32 accumulation), and the row maximum is
+// The bound is a dense [rows x 256] x [256 x 16] product per tile of 16 blocks
+// (score_core.h: [q+ | q-] . [kmax ; kmin], exact bf16 operands, fp32
+// accumulation on v_mfma_f32_16x16x32_bf16) for the 5 to 64 rows of a KV head
+// (fewer go to the vector-ALU scorer of score_valu.hip), and the row maximum is
 // taken in the epilogue with two cross-lane exchanges.
 //
 // Memory: every summary byte is read once. A wave owns TPW consecutive tiles
@@ -25,6 +22,7 @@
 // (8 x 131,072 tokens, 268 MB) 48.6 us against 49.9 us (fewer query reads;
 // 3, 5, 6 and 8 summary tiles per wave: 48.6, 50.8, 51.7 and 56.6 us).
 #include "oasis_internal.h"
+#include "score_core.h"
 
 namespace oasis {
 
@@ -48,47 +46,20 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   const Ctx c = ctx_blocks(a.ctx_len[r], a.B, a.NBmax);
   const int ntiles = (a.NBmax + 15) >> 4;
   const int tile0 = (blockIdx.x * 4 + wave) * TPW;
-  // [row tile][k-step][q+ / q-][lane]: 16 bytes each
-  __shared__ u32x4 s_q[NRT][4][2][64];
+  __shared__ ScoreQOperands<NRT> s_q;
 
   // queries first (cache-resident, needed first), then the summaries of all TPW tiles
-  const int nrows = a.num_draft * a.G;
   u32x4 qraw[NRT];
 #pragma unroll
-  for (int j = 0; j < NRT; ++j) {
-    const int e = threadIdx.x + j * 256;  // (row tile, k-step, lane) of the operand this thread builds
-    const int v = e >> 8;
-    const int st = (e >> 6) & 3;
-    const int el = e & 63;
-    int row = v * 16 + (el & 15);
-    if (row >= nrows) row = 0;  // rows past the last repeat row 0: the maximum is unchanged
-    const int t = a.first_draft + row / a.G;
-    const int qh = h * a.G + row % a.G;
-    qraw[j] = ldg16(a.q + (((long long)r * a.T + t) * a.Hq + qh) * kHeadDim + st * 32 + (el >> 4) * 8);
-  }
+  for (int j = 0; j < NRT; ++j) qraw[j] = score_q_raw(a, r, h, threadIdx.x + j * 256);
   const long long sum_base = (long long)rh * a.NBmax * kHeadDim;
   const uint16_t* kmx = a.kmax + sum_base;
   const uint16_t* kmn = a.kmin + sum_base;
   u32x4 vmax[TPW][4], vmin[TPW][4];
 #pragma unroll
-  for (int t = 0; t < TPW; ++t) {
-    const int blk = (tile0 + t) * 16 + n;
-    const bool live = blk < c.n_cand;
+  for (int t = 0; t < TPW; ++t) score_tile_load(kmx, kmn, tile0 + t, c.n_cand, g, n, vmax[t], vmin[t]);
 #pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      const long long off = (long long)blk * kHeadDim + st * 32 + g * 8;
-      vmax[t][st] = live ? ldg16(kmx + off) : u32x4{0, 0, 0, 0};
-      vmin[t][st] = live ? ldg16(kmn + off) : u32x4{0, 0, 0, 0};
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < NRT; ++j) {
-    const int e = threadIdx.x + j * 256;
-    u32x4 p, m;
-    split_sign(qraw[j], p, m);
-    s_q[e >> 8][(e >> 6) & 3][0][e & 63] = p;
-    s_q[e >> 8][(e >> 6) & 3][1][e & 63] = m;
-  }
+  for (int j = 0; j < NRT; ++j) score_q_store<NRT>(s_q, threadIdx.x + j * 256, qraw[j]);
   __syncthreads();  // every wave reaches it: waves past the last tile return only below
   if (tile0 >= ntiles) return;
 
@@ -99,23 +70,9 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
 #pragma unroll
     for (int v = 0; v < NRT; ++v) {
       bf16x8 ap[4], an[4];
+      score_q_tile<NRT>(s_q, v, lane, ap, an);
 #pragma unroll
-      for (int st = 0; st < 4; ++st) {
-        ap[st] = as_bf16x8(s_q[v][st][0][lane]);
-        an[st] = as_bf16x8(s_q[v][st][1][lane]);
-      }
-#pragma unroll
-      for (int t = 0; t < TPW; ++t) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap[st], as_bf16x8(vmax[t][st]), acc, 0, 0, 0);
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(an[st], as_bf16x8(vmin[t][st]), acc, 0, 0, 0);
-        // lane (g, n) holds rows 4g..4g+3 of the row tile for block n of tile t
-        best[t] = fmaxf(best[t], fmaxf(fmaxf(acc[0], acc[1]), fmaxf(acc[2], acc[3])));
-      }
+      for (int t = 0; t < TPW; ++t) best[t] = score_tile_fold(ap, an, vmax[t], vmin[t], best[t]);
     }
   }
   float* srow = a.scores + (long long)rh * a.NBmax;
@@ -123,8 +80,7 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   for (int t = 0; t < TPW; ++t) {
     const int tile = tile0 + t;
     if (tile >= ntiles) break;
-    float b = fmaxf(best[t], __shfl_xor(best[t], 16));
-    b = fmaxf(b, __shfl_xor(b, 32));
+    const float b = score_lane_reduce(best[t]);
     const int blk = tile * 16 + n;
     if (g == 0 && blk < a.NBmax) srow[blk] = blk < c.n_cand ? b : -INFINITY;
   }

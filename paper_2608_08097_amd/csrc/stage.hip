@@ -50,6 +50,7 @@
 #include <climits>
 
 #include "oasis_internal.h"
+#include "score_core.h"
 #include "select.h"
 
 namespace oasis {
@@ -612,7 +613,120 @@ __global__ __launch_bounds__(kSelThreads) void topk_plan_kernel(TopkArgs t, Stag
   plan_pass<kSelThreads>(a, rh, 1, 1, s_slot, s_page, s_epair, s_prh, s_wave, s_lsel, m);
 }
 
+// Scoring, top-K and, with PLAN, the transfer plan of one (request, KV head) in
+// one workgroup of kScoreSelThreads threads (paper §4.2.1: the draft rows rank
+// every block of the head; §4.2.2: top-K prediction; §4.2.3: delta selection).
+// The workgroup scores its row's candidate tiles with the scorer's MFMA pieces
+// (score_core.h, so the scores are bit-identical to the scoring kernel's),
+// writes the row of scores, and selects from it after a workgroup barrier, so
+// no other workgroup is waited for. The query operands sit in the selection's
+// key staging area until the selection starts. Each wave scores kScoreSelTiles
+// tiles at a time, all their loads issued before the first MFMA. Small
+// workgroups let several rows share a CU, so that one row's selection overlaps
+// another's loads. Worth trying where the rows are many and short, so that one
+// workgroup per row fills the chip; with few long rows the two kernels spread
+// a row over many workgroups.
+constexpr int kScoreSelThreads = 256;
+constexpr int kScoreSelTiles = 4;
+
+template <int NRT, int KPT, bool PLAN>
+__global__ __launch_bounds__(kScoreSelThreads) void score_select_kernel(ScoreArgs sa, TopkArgs t, StageArgs a) {
+  constexpr int NTHR = kScoreSelThreads;
+  constexpr int TPW = kScoreSelTiles;
+  __shared__ __align__(16) SelectShared<NTHR, KPT> sh;
+  __shared__ int s_lsel[PLAN ? kMaxK : 1];
+  __shared__ int s_slot[PLAN ? kMaxK + kMaxPairs : 1], s_page[PLAN ? kMaxK + kMaxPairs : 1];
+  __shared__ int s_epair[PLAN ? kMaxK + kMaxPairs : 1];
+  __shared__ int s_prh[PLAN ? kMaxPairs : 1];
+  __shared__ int s_wave[NTHR / 64 + 1];
+  static_assert(sizeof(ScoreQOperands<NRT>) <= sizeof(sh.keys), "query operands must fit the key staging area");
+  const int rh = blockIdx.x;
+  const int r = rh / sa.Hkv;
+  const int h = rh - r * sa.Hkv;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4;
+  const int n = lane & 15;
+  const Ctx c = ctx_blocks(sa.ctx_len[r], sa.B, sa.NBmax);
+  ScoreQOperands<NRT>& s_q = *reinterpret_cast<ScoreQOperands<NRT>*>(sh.keys);
+  for (int e = threadIdx.x; e < NRT * 256; e += NTHR) score_q_store<NRT>(s_q, e, score_q_raw(sa, r, h, e));
+
+  const long long sum_base = (long long)rh * sa.NBmax * kHeadDim;
+  const uint16_t* kmx = sa.kmax + sum_base;
+  const uint16_t* kmn = sa.kmin + sum_base;
+  float* srow = sa.scores + (long long)rh * sa.NBmax;
+  const int ntile_c = (c.n_cand + 15) >> 4;
+  __syncthreads();  // query operands are in
+  for (int tile0 = wave * TPW; tile0 < ntile_c; tile0 += (NTHR / 64) * TPW) {
+    u32x4 vmax[TPW][4], vmin[TPW][4];
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) score_tile_load(kmx, kmn, tile0 + u, c.n_cand, g, n, vmax[u], vmin[u]);
+    float best[TPW];
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) best[u] = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < NRT; ++v) {
+      bf16x8 ap[4], an[4];
+      score_q_tile<NRT>(s_q, v, lane, ap, an);
+#pragma unroll
+      for (int u = 0; u < TPW; ++u) best[u] = score_tile_fold(ap, an, vmax[u], vmin[u], best[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) {
+      const float b = score_lane_reduce(best[u]);
+      const int blk = (tile0 + u) * 16 + n;
+      if (g == 0 && blk < c.n_cand) srow[blk] = b;
+    }
+  }
+  for (int b = c.n_cand + threadIdx.x; b < sa.NBmax; b += NTHR) srow[b] = -INFINITY;
+  __syncthreads();  // the score row is complete, and the query operands are no longer read
+  select_row<NTHR, KPT>(srow, c.n_cand, t.k, t.sel + (long long)rh * t.k, t.sel_count + rh, sh,
+                        PLAN ? s_lsel : nullptr);
+  if (PLAN) {
+    __syncthreads();
+    const int m = c.n_cand < t.k ? (c.n_cand > 0 ? c.n_cand : 0) : t.k;
+    plan_pass<NTHR>(a, rh, 1, 1, s_slot, s_page, s_epair, s_prh, s_wave, s_lsel, m);
+  }
+}
+
+template <int NRT, int KPT>
+hipError_t launch_score_select_t(const ScoreArgs& sa, const TopkArgs& t, const StageArgs* plan, hipStream_t s,
+                                 const LaunchTiming& lt) {
+  const dim3 grid((unsigned)(sa.R * sa.Hkv));
+  if (plan)
+    launch_kernel(score_select_kernel<NRT, KPT, true>, grid, dim3(kScoreSelThreads), s, lt, sa, t, *plan);
+  else
+    launch_kernel(score_select_kernel<NRT, KPT, false>, grid, dim3(kScoreSelThreads), s, lt, sa, t, StageArgs{});
+  return hipGetLastError();
+}
+
+template <int NRT>
+hipError_t launch_score_select_nrt(const ScoreArgs& sa, const TopkArgs& t, const StageArgs* plan, hipStream_t s,
+                                   const LaunchTiming& lt) {
+  // keys per thread; the staged keys also hold the query operands (8 KiB per row tile)
+  const int per = (sa.NBmax + kScoreSelThreads - 1) / kScoreSelThreads;
+  if constexpr (NRT == 1) {
+    if (per <= 8) return launch_score_select_t<NRT, 8>(sa, t, plan, s, lt);
+  }
+  if (per <= 16) return launch_score_select_t<NRT, 16>(sa, t, plan, s, lt);
+  if (per <= 32) return launch_score_select_t<NRT, 32>(sa, t, plan, s, lt);
+  return launch_score_select_t<NRT, 64>(sa, t, plan, s, lt);
+}
+
 }  // namespace
+
+bool score_select_supported(const ScoreArgs& sa) {
+  const int rows = sa.num_draft * sa.G;
+  return rows > kScoreValuMaxRows && rows <= kScoreSelectMaxRows && sa.NBmax <= kScoreSelectMaxBlocks;
+}
+
+hipError_t launch_score_select(const ScoreArgs& sa, const TopkArgs& t, const StageArgs* plan, hipStream_t s,
+                               const LaunchTiming& lt) {
+  if (!score_select_supported(sa)) return hipErrorInvalidValue;
+  if (plan && (plan->mode != kStagePlanOnly || !plan->ws || plan->local_only)) return hipErrorInvalidValue;
+  return (sa.num_draft * sa.G + 15) / 16 == 1 ? launch_score_select_nrt<1>(sa, t, plan, s, lt)
+                                               : launch_score_select_nrt<2>(sa, t, plan, s, lt);
+}
 
 template <int BS>
 hipError_t launch_bs(const StageArgs& a, hipStream_t s, const LaunchTiming& t) {

@@ -123,6 +123,25 @@ def test_pipeline_argument_checks_without_gpu(lib):
     L.oasis_pipeline_destroy(None)
 
 
+def test_score_select_checks_without_gpu(lib):
+    """The fused score + select entry point rejects the sizes it does not cover before any HIP call."""
+    L = lib.lib()
+    P = [ctypes.c_void_p(64 * (i + 1)) for i in range(6)]  # non-NULL stand-ins, never dereferenced
+    ok = lib.dims(2, 32, 8, 128, 16, 512)
+    # 4 scoring rows (G = 4, one draft): the vector-ALU scorer's range
+    assert L.oasis_score_select(ctypes.byref(ok), P[0], 2, 1, 1, P[1], P[2], P[3], 64, P[4], P[5], P[0], None) == 2
+    assert "scoring rows" in lib.oasis_last_error()
+    # 40 scoring rows (G = 8, five drafts)
+    g8 = lib.dims(2, 64, 8, 128, 16, 512)
+    assert L.oasis_score_select(ctypes.byref(g8), P[0], 6, 1, 5, P[1], P[2], P[3], 64, P[4], P[5], P[0], None) == 2
+    long_rows = lib.dims(2, 32, 8, 128, 16, 20000)
+    assert L.oasis_score_select(ctypes.byref(long_rows), P[0], 5, 1, 4, P[1], P[2], P[3], 64, P[4], P[5], P[0],
+                                None) == 2
+    assert "max_blocks" in lib.oasis_last_error()
+    assert L.oasis_score_select(ctypes.byref(ok), None, 5, 1, 4, P[1], P[2], P[3], 64, P[4], P[5], P[0], None) == 1
+    assert L.oasis_pipeline_set_fused_prediction(None, 0) == 1
+
+
 def test_workspace_sizes(lib):
     d = lib.dims(8, 32, 8, 128, 16, 8192)
     ws = lib.oasis_attn_workspace_bytes(d, 5, 128)

@@ -146,6 +146,55 @@ def test_scores_rows(seed, R, Hq, Hkv, T, first_draft, num_draft, NB, B, lens):
     assert_scores_close(scores.cpu().numpy(), ref)
 
 
+SCORE_SELECT_CASES = [
+    # (seed, R, Hq, Hkv, T, first_draft, num_draft, NBmax, B, ctx lengths, k, tied): rows = G * num_draft, 5 to 32
+    (1, 2, 40, 8, 2, 1, 1, 257, 16, [4112, 4000], 64, False),              # 5 rows
+    (2, 3, 32, 8, 5, 1, 4, 700, 16, [11200, 16 * 300 + 5, 0], 128, False),  # 16 rows, ragged, an empty context
+    (3, 2, 24, 8, 4, 1, 3, 300, 16, [4800, 2222], 128, True),              # 9 rows, duplicated blocks (ties)
+    (4, 1, 17, 1, 2, 1, 1, 1000, 16, [16000], 200, False),                 # 17 rows: two row tiles
+    (5, 2, 64, 8, 5, 1, 4, 150, 32, [4800, 1234], 32, True),               # 32 rows, B = 32
+    (6, 2, 32, 8, 5, 1, 4, 9000, 16, [144000, 100000], 128, False),        # > 8 keys per thread
+    (7, 2, 32, 8, 5, 1, 4, 64, 16, [1024, 700], 128, False),               # fewer candidates than k
+]
+
+
+@pytest.mark.parametrize("seed,R,Hq,Hkv,T,first_draft,num_draft,NB,B,lens,k,tied", SCORE_SELECT_CASES)
+def test_score_select_fused(seed, R, Hq, Hkv, T, first_draft, num_draft, NB, B, lens, k, tied):
+    """The fused score + select kernel gives bit for bit the scores and selections of the two kernels,
+    and the selection matches the oracle's under the near-tie rule."""
+    d_head = 128
+    q = random_bf16(600 + seed, (R, T, Hq, d_head))
+    a = random_bf16(610 + seed, (R, Hkv, NB, d_head))
+    b = random_bf16(620 + seed, (R, Hkv, NB, d_head), scale=2.0)
+    if tied:  # many blocks share one summary: equal scores, broken by block id
+        a = a[:, :, np.arange(NB) % 7]
+        b = b[:, :, np.arange(NB) % 7]
+    av, bv = O.bf16_to_f64(a), O.bf16_to_f64(b)
+    kmax_bits = np.ascontiguousarray(np.where(av >= bv, a, b))
+    kmin_bits = np.ascontiguousarray(np.where(av >= bv, b, a))
+    ctx = np.array(lens, np.int32)
+    note(f"score+select rows={Hq // Hkv * num_draft} seed={seed} NB={NB} k={k}")
+    d = P.dims(R, Hq, Hkv, d_head, B, NB)
+    args = (dev_bf16(q), T, first_draft, num_draft, dev_bf16(kmax_bits), dev_bf16(kmin_bits), dev_i32(ctx))
+    s2 = torch.full((R, Hkv, NB), 7.0, device="cuda")
+    sel2 = torch.full((R, Hkv, k), -7, dtype=torch.int32, device="cuda")
+    cnt2 = torch.full((R, Hkv), -7, dtype=torch.int32, device="cuda")
+    P.oasis_score_blocks(d, *args, s2)
+    P.oasis_select_topk(d, s2, args[-1], k, sel2, cnt2)
+    s1 = torch.full((R, Hkv, NB), 5.0, device="cuda")
+    sel1 = torch.full((R, Hkv, k), -5, dtype=torch.int32, device="cuda")
+    cnt1 = torch.full((R, Hkv), -5, dtype=torch.int32, device="cuda")
+    P.oasis_score_select(d, *args, k, s1, sel1, cnt1)
+    torch.cuda.synchronize()
+    assert np.array_equal(s1.cpu().numpy(), s2.cpu().numpy()), "scores differ from the scoring kernel"
+    assert np.array_equal(sel1.cpu().numpy(), sel2.cpu().numpy()), "selection differs from the top-K kernel"
+    assert np.array_equal(cnt1.cpu().numpy(), cnt2.cpu().numpy())
+    ref = O.block_scores(q, O.bf16_to_f64(kmax_bits), O.bf16_to_f64(kmin_bits), ctx, Hkv, B, first_draft, num_draft)
+    assert_scores_close(s1.cpu().numpy(), ref)
+    ref_sel, ref_cnt = O.select_topk(ref, ctx, k, B)
+    selection_diff(sel1.cpu().numpy(), cnt1.cpu().numpy(), ref_sel, ref_cnt, ref)
+
+
 SELECT_CASES = [
     # (seed, R, H, NBmax, B, ctx lengths, k, n_distinct)
     (1, 3, 8, 700, 16, [16 * 700, 16 * 300 + 5, 16 * 129], 128, None),
@@ -514,11 +563,13 @@ def test_pipelined_multistep(cap, issue):
 
 
 @pytest.mark.parametrize("plan_pred", [False, True])
-def test_pipelined_layers_native(plan_pred):
+@pytest.mark.parametrize("fused", [False, True])
+def test_pipelined_layers_native(plan_pred, fused):
     """Several layers interleaved on the native issuer with no host synchronization
     between steps (paper §4.2.2: per-layer chains, layer-local waits); every
     layer's final state equals its own oracle chain, with the transfer planned on
-    either stream."""
+    either stream, and the prediction by the separate kernels or by the fused
+    score + select (+ plan) kernel."""
     n_layers, rounds, cap = 3, 4, 3
     w = make_workload("c2", num_reqs=3, ctx_args=(900, 2500), budget=16 * 20, ar_queries=True)
     c = w.cfg
@@ -530,7 +581,8 @@ def test_pipelined_layers_native(plan_pred):
     ctx_d = dev_i32(ctx)
     qs = [w.layer_queries(l, rounds + 1) for l in range(n_layers)]
     kmax, kmin = O.block_summaries(hk, w.block_table, ctx, c.block_size, w.NBmax)
-    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap, plan_on_prediction=plan_pred)
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap, plan_on_prediction=plan_pred,
+                      fused_prediction=P.FUSED_PREDICTION_ON if fused else P.FUSED_PREDICTION_OFF)
     layers = [LayerState(d, c.T, k) for _ in range(n_layers)]
     ref = []
     for l, st in enumerate(layers):
@@ -547,7 +599,7 @@ def test_pipelined_layers_native(plan_pred):
         O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, 0, pk, pv, ctx, c.block_size)
         ref.append(dict(smap=smap, stamp=stamp, pk=pk, pv=pv))
     q_dev = [[dev_bf16(x) for x in qs[l]] for l in range(n_layers)]
-    note(f"native pipelined layers: issuing (plan on prediction: {plan_pred})")
+    note(f"native pipelined layers: issuing (plan on prediction: {plan_pred}, fused prediction: {fused})")
     for s in range(1, rounds + 1):
         for l in range(n_layers):
             path.step_pipelined(layers[l], q_dev[l][s], ctx_d, s)

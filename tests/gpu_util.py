@@ -120,6 +120,46 @@ def selection_diff(sel_gpu, cnt_gpu, sel_ref, cnt_ref, scores_ref):
     return swapped
 
 
+def adjudicate_capped(sel_g, cnt_g, smap_before, smap_after_g, scores_ref, sel_ref, cnt_ref, cap):
+    """The near-tie rule of a capped delta step (reading R22), applied to one GPU step.
+
+    The GPU ranks by its fp32 scores, the oracle by float64 ones. The GPU's
+    selection must match the oracle's under the selection rule (swaps only
+    within TIE_REL of the cut). Its admission under the cap (the blocks newly
+    resident in ``smap_after_g`` compared with ``smap_before``) must equal the
+    ``cap`` highest-scoring misses of that selection, except for blocks whose
+    oracle score is within TIE_REL * max(|tau_C|, 1) of tau_C, the oracle's
+    C-th admitted score. Returns the scores with which the oracle, given the
+    GPU's selection, admits exactly the GPU's choice (the oracle's own scores
+    wherever the two agree), so that the rest of the step (victims, slot map,
+    stamps, pools) is then compared bit for bit.
+    """
+    selection_diff(sel_g, cnt_g, sel_ref, cnt_ref, scores_ref)
+    use = np.array(scores_ref, dtype=np.float64, copy=True)
+    R, H, _ = smap_before.shape
+    for r in range(R):
+        for h in range(H):
+            m = int(cnt_g[r, h])
+            resident = {int(b) for b in smap_before[r, h] if b >= 0}
+            misses = [int(b) for b in sel_g[r, h, :m] if int(b) not in resident]
+            if cap is None or len(misses) <= cap:
+                continue
+            s = use[r, h]
+            ranked = sorted(misses, key=lambda b: (-s[b], b))
+            adm_ref = set(ranked[:cap])
+            tau = s[ranked[cap - 1]]
+            adm_g = {int(b) for b in smap_after_g[r, h] if b >= 0} - resident
+            assert len(adm_g) == cap, f"({r},{h}): {len(adm_g)} admitted under a cap of {cap}"
+            tol = TIE_REL * max(abs(tau), 1.0)
+            for x in adm_g ^ adm_ref:
+                assert abs(s[x] - tau) <= tol, f"({r},{h}) block {x}: score {s[x]} vs admission cut {tau}"
+            if adm_g != adm_ref:
+                top = np.max(s[np.isfinite(s)]) + 1.0
+                for x in adm_g:
+                    s[x] = top
+    return use
+
+
 def oracle_layer(w: Workload, host_k: np.ndarray, host_v: np.ndarray, ctx: np.ndarray, q: np.ndarray, k: int):
     """Oracle pipeline for one step from a cold working set: summaries, scores, selection, staging, attention."""
     c = w.cfg

@@ -13,8 +13,8 @@ import torch
 from oracle import oasis_oracle as O
 from paper_2608_08097_amd.path import DecodePath, LayerState, dense_working_set
 import paper_2608_08097_amd as P
-from tests.gpu_util import (assert_attn_close, assert_lse_close, assert_scores_close, as_np_bits, dev_bf16,
-                            dev_i32, host_bits, note, pinned_pages, selection_diff)
+from tests.gpu_util import (adjudicate_capped, assert_attn_close, assert_lse_close, assert_scores_close, as_np_bits,
+                            dev_bf16, dev_i32, host_bits, note, pinned_pages, pool_v_from_htd, selection_diff)
 from workloads import config, Workload
 
 pytestmark = pytest.mark.gpu
@@ -116,7 +116,10 @@ def test_fullsize_dense_c4():
 
 
 def test_fullsize_pipelined_capped_c4():
-    """The benchmark's loop: 8 x 131,072 tokens, budget 2,048, fetch cap 6, two layer states."""
+    """The benchmark's loop: 8 x 131,072 tokens, budget 2,048, fetch cap 6, two layer states, issued through
+    the native pipeline and read back after every step. A sampled request follows its oracle chain step by
+    step; near ties at the selection cut or at the cap's admission cut are adjudicated by the tie rule and
+    the oracle then continues from the GPU's choice (reading R22)."""
     NL, S, cap = 2, 4, 6
     w, hk_t, hv_t = _tier("c4", ar_queries=True)
     c = w.cfg
@@ -134,42 +137,57 @@ def test_fullsize_pipelined_capped_c4():
     for l, st in enumerate(layers):
         path.predict(st, q_dev[l][0], ctx_d)
         path.stage(st, ctx_d, 0, fetch_cap=K)
-    note("full-size pipelined c4: issuing")
-    for i in range(NL * S):
-        path.step_pipelined(layers[i % NL], q_dev[i % NL][i // NL], ctx_d, i)
-    path.join()
     torch.cuda.synchronize()
     hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
     r = 5
     bt, cr = w.block_table[r:r + 1], ctx[r:r + 1]
     kmax, kmin = O.block_summaries(hk, bt, cr, B, w.NBmax)
-    for l, st in enumerate(layers):
+    ref = []
+    for l, st in enumerate(layers):   # the uncapped fill, on the GPU's selection (adjudicated)
         smap = np.full((1, H, K), -1, np.int32)
         stamp = np.zeros_like(smap)
         pk = np.zeros((1, K + 1, H, B, c.head_dim), np.uint16)
         pv = np.zeros_like(pk)
         s0 = O.block_scores(qs[l][0][r:r + 1], kmax, kmin, cr, H, B)
         sel, cnt = O.select_topk(s0, cr, K, B)
-        O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, 0, pk, pv, cr, B)
-        for i in range(l, NL * S, NL):
-            qr = qs[l][i // NL][r:r + 1]
-            ref_o, ref_l = O.sparse_attend(qr, pk, pv, smap, cr, B)
-            s = O.block_scores(qr, kmax, kmin, cr, H, B)
-            sel, cnt = O.select_topk(s, cr, K, B)
-            O.stage_blocks(hk, hv, bt, sel, cnt, smap, stamp, i, pk, pv, cr, B, scores=s, fetch_cap=cap)
-        assert not selection_diff(st.sel.cpu().numpy()[r:r + 1], st.sel_count.cpu().numpy()[r:r + 1], sel, cnt, s)
+        sel_g, cnt_g = st.sel.cpu().numpy()[r:r + 1], st.sel_count.cpu().numpy()[r:r + 1]
+        selection_diff(sel_g, cnt_g, sel, cnt, s0)
+        O.stage_blocks(hk, hv, bt, sel_g, cnt_g, smap, stamp, 0, pk, pv, cr, B)
         assert np.array_equal(st.slot_map.cpu().numpy()[r:r + 1], smap), l
-        assert np.array_equal(st.slot_stamp.cpu().numpy()[r:r + 1], stamp), l
-        assert_attn_close(host_bits(st.out)[r:r + 1], ref_o, f"layer {l}")
+        ref.append(dict(smap=smap, stamp=stamp, pk=pk, pv=pv))
+    for i in range(NL * S):
+        l = i % NL
+        st, o = layers[l], ref[l]
+        note(f"full-size pipelined c4: step {i} (layer {l})")
+        path.step_pipelined(st, q_dev[l][i // NL], ctx_d, i)
+        path.join()
+        torch.cuda.synchronize()
+        qr = qs[l][i // NL][r:r + 1]
+        ref_o, ref_l = O.sparse_attend(qr, o["pk"], o["pv"], o["smap"], cr, B)
+        assert_attn_close(host_bits(st.out)[r:r + 1], ref_o, f"step {i} layer {l}")
         assert_lse_close(st.lse.cpu().numpy()[r:r + 1], ref_l)
+        sc = O.block_scores(qr, kmax, kmin, cr, H, B)
+        sel, cnt = O.select_topk(sc, cr, K, B)
+        sel_g, cnt_g = st.sel.cpu().numpy()[r:r + 1], st.sel_count.cpu().numpy()[r:r + 1]
+        smap_g = st.slot_map.cpu().numpy()[r:r + 1]
+        use = adjudicate_capped(sel_g, cnt_g, o["smap"], smap_g, sc, sel, cnt, cap)
+        O.stage_blocks(hk, hv, bt, sel_g, cnt_g, o["smap"], o["stamp"], i, o["pk"], o["pv"], cr, B, scores=use,
+                       fetch_cap=cap)
+        assert np.array_equal(smap_g, o["smap"]), (i, l)
+        assert np.array_equal(st.slot_stamp.cpu().numpy()[r:r + 1], o["stamp"]), (i, l)
+    for l, st in enumerate(layers):
+        assert np.array_equal(host_bits(st.pool_k)[r:r + 1, :K], ref[l]["pk"][:, :K]), l
+        assert np.array_equal(host_bits(st.pool_v)[r:r + 1, :K], pool_v_from_htd(ref[l]["pv"])[:, :K]), l
     path.close()
 
 
 @pytest.mark.parametrize("plan_pred", [False, True])
 def test_fullsize_growing_c3(plan_pred):
     """The reasoning loop: 64 requests (1K prompt + 4K-16K generated), one token per step, summary
-    updates on block completion, two layer states; a sampled request against its oracle chain. The
-    benchmark plans this loop's transfers on the prediction stream (``plan_pred``)."""
+    updates on block completion, two layer states; read back after every step, a sampled request follows
+    its oracle chain under the tie rule (reading R22). The benchmark plans this loop's transfers on the
+    prediction stream (``plan_pred``); with 512 (request, KV head) pairs the prediction runs as the fused
+    score + select (+ plan) kernel."""
     NL, S, cap = 2, 20, 6
     w, hk_t, hv_t = _tier("c3", steps=S)
     c = w.cfg
@@ -183,39 +201,43 @@ def test_fullsize_growing_c3(plan_pred):
     layers = [path.new_layer() for _ in range(NL)]
     for st in layers:
         path.build_summaries(st, ctx_dev[0])
-    note(f"full-size growing c3 (plan on prediction: {plan_pred}): issuing")
-    for s in range(S):
-        for l, st in enumerate(layers):
-            if s:
-                P.oasis_update_summaries(d, hk_t, bt, ctx_dev[s - 1], ctx_dev[s], 1, st.kmax, st.kmin)
-            path.step_pipelined(st, q_dev[l][s], ctx_dev[s], s, growing=True)
-    path.join()
     torch.cuda.synchronize()
     hk, hv = as_np_bits(hk_t), as_np_bits(hv_t)
     r = int(np.argmax(w.ctx0 % B))                     # a request whose local block is far from full
     brow = w.block_table[r:r + 1]
     none_sel = np.full((1, H, K), -1, np.int32)
     zero_cnt = np.zeros((1, H), np.int32)
-    for l, st in enumerate(layers):
-        smap = np.full((1, H, K), -1, np.int32)
-        stamp = np.zeros_like(smap)
-        pk = np.zeros((1, K + 1, H, B, c.head_dim), np.uint16)
-        pv = np.zeros_like(pk)
-        c0 = w.ctx_len(0)[r:r + 1]
+    c0 = w.ctx_len(0)[r:r + 1]
+    ref = []
+    for l in range(NL):
         kmax, kmin = O.block_summaries(hk, brow, c0, B, w.NBmax)
-        for s in range(S):
-            cr = w.ctx_len(s)[r:r + 1]
+        smap = np.full((1, H, K), -1, np.int32)
+        ref.append(dict(kmax=kmax, kmin=kmin, smap=smap, stamp=np.zeros_like(smap),
+                        pk=np.zeros((1, K + 1, H, B, c.head_dim), np.uint16),
+                        pv=np.zeros((1, K + 1, H, B, c.head_dim), np.uint16)))
+    note(f"full-size growing c3 (plan on prediction: {plan_pred}): issuing")
+    for s in range(S):
+        cr = w.ctx_len(s)[r:r + 1]
+        for l, st in enumerate(layers):
+            o = ref[l]
             if s:
-                O.update_summaries(hk, brow, w.ctx_len(s - 1)[r:r + 1], cr, B, kmax, kmin, 1)
-            O.stage_blocks(hk, hv, brow, none_sel, zero_cnt, smap, stamp, s, pk, pv, cr, B)
+                P.oasis_update_summaries(d, hk_t, bt, ctx_dev[s - 1], ctx_dev[s], 1, st.kmax, st.kmin)
+                O.update_summaries(hk, brow, w.ctx_len(s - 1)[r:r + 1], cr, B, o["kmax"], o["kmin"], 1)
+            path.step_pipelined(st, q_dev[l][s], ctx_dev[s], s, growing=True)
+            path.join()
+            torch.cuda.synchronize()
+            O.stage_blocks(hk, hv, brow, none_sel, zero_cnt, o["smap"], o["stamp"], s, o["pk"], o["pv"], cr, B)
             qr = qs[l][s][r:r + 1]
-            ref_o, ref_l = O.sparse_attend(qr, pk, pv, smap, cr, B)
-            sc = O.block_scores(qr, kmax, kmin, cr, H, B)
+            ref_o, ref_l = O.sparse_attend(qr, o["pk"], o["pv"], o["smap"], cr, B)
+            assert_attn_close(host_bits(st.out)[r:r + 1], ref_o, f"step {s} layer {l}")
+            assert_lse_close(st.lse.cpu().numpy()[r:r + 1], ref_l)
+            sc = O.block_scores(qr, o["kmax"], o["kmin"], cr, H, B)
             sel, cnt = O.select_topk(sc, cr, K, B)
-            O.stage_blocks(hk, hv, brow, sel, cnt, smap, stamp, s, pk, pv, cr, B, copy_local=False, scores=sc,
-                           fetch_cap=cap)
-        assert not selection_diff(st.sel.cpu().numpy()[r:r + 1], st.sel_count.cpu().numpy()[r:r + 1], sel, cnt, sc)
-        assert np.array_equal(st.slot_map.cpu().numpy()[r:r + 1], smap), l
-        assert_attn_close(host_bits(st.out)[r:r + 1], ref_o, f"layer {l}")
-        assert_lse_close(st.lse.cpu().numpy()[r:r + 1], ref_l)
+            sel_g, cnt_g = st.sel.cpu().numpy()[r:r + 1], st.sel_count.cpu().numpy()[r:r + 1]
+            smap_g = st.slot_map.cpu().numpy()[r:r + 1]
+            use = adjudicate_capped(sel_g, cnt_g, o["smap"], smap_g, sc, sel, cnt, cap)
+            O.stage_blocks(hk, hv, brow, sel_g, cnt_g, o["smap"], o["stamp"], s, o["pk"], o["pv"], cr, B,
+                           copy_local=False, scores=use, fetch_cap=cap)
+            assert np.array_equal(smap_g, o["smap"]), (s, l)
+            assert np.array_equal(st.slot_stamp.cpu().numpy()[r:r + 1], o["stamp"]), (s, l)
     path.close()

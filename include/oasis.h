@@ -79,7 +79,7 @@
 extern "C" {
 #endif
 
-#define OASIS_ABI_VERSION 6
+#define OASIS_ABI_VERSION 7
 
 /* Only the entry points below are exported from liboasis.so. */
 #if defined(__GNUC__) || defined(__clang__)
@@ -308,7 +308,7 @@ OASIS_API oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const ui
  * that must not call the allocator, harnesses that forbid it). Same operation,
  * arguments, layouts and checks as oasis_sparse_decode_attn; the split partials
  * go to a scratch array of the library in device memory: OASIS_NOALLOC_SCRATCH_BYTES
- * (32 MiB) per GPU, held from the library's load until the process ends. Sizes
+ * (16 MiB) per GPU, held from the library's load until the process ends. Sizes
  * whose oasis_attn_workspace_bytes exceeds it return OASIS_ERR_UNSUPPORTED
  * without launching. Nothing is allocated, on the host or the device; the first
  * call on a device looks up the scratch array's address there (one runtime
@@ -318,7 +318,7 @@ OASIS_API oasis_status oasis_sparse_decode_attn(const oasis_dims* dims, const ui
  * one stream. The scratch needs no clearing between calls (each call writes the
  * partials it reads).
  */
-#define OASIS_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+#define OASIS_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
 OASIS_API oasis_status oasis_sparse_decode_attn_noalloc(const oasis_dims* dims, const uint16_t* q,
                                               int32_t num_q_tokens, const uint16_t* pool_k,
                                               const uint16_t* pool_v, const int32_t* slot_map, int32_t k_slots,

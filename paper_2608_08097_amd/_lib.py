@@ -60,7 +60,7 @@ def dims(num_reqs, num_q_heads, num_kv_heads, head_dim, block_size, max_blocks) 
 
 
 _lib = None
-ABI_VERSION = 6  # OASIS_ABI_VERSION of include/oasis.h
+ABI_VERSION = 7  # OASIS_ABI_VERSION of include/oasis.h
 
 _P = ctypes.c_void_p
 _I32 = ctypes.c_int32
@@ -345,7 +345,7 @@ def oasis_sparse_decode_attn(d: OasisDims, q, num_q_tokens: int, pool_k, pool_v,
         int(workspace.numel()) if workspace is not None else 0, _stream(stream)))
 
 
-NOALLOC_SCRATCH_BYTES = 32 << 20  # OASIS_NOALLOC_SCRATCH_BYTES of include/oasis.h
+NOALLOC_SCRATCH_BYTES = 16 << 20  # OASIS_NOALLOC_SCRATCH_BYTES of include/oasis.h
 
 
 def oasis_sparse_decode_attn_noalloc(d: OasisDims, q, num_q_tokens: int, pool_k, pool_v, slot_map, k_slots: int,

@@ -29,7 +29,13 @@
 // So K and V go straight from HBM into MFMA registers with 16-byte loads and
 // no LDS round trip; every lane owns one query row, so the running max and sum
 // need only two cross-lane exchanges per unit.
+//
+// With more than two row tiles (G * T > 32 rows) the registers of one wave no
+// longer hold every tile's accumulators next to two units of K and V; there a
+// workgroup has one wave per row tile and the unit's K and V cross HBM once,
+// into LDS, for all of them (attn_split_rows_kernel).
 #include <mutex>
+#include <utility>
 
 #include "oasis_internal.h"
 
@@ -37,10 +43,10 @@ namespace oasis {
 namespace {
 
 constexpr int kW = 4;  // waves per workgroup
-// Workgroups of one attention call: one per CU when the kernel prefetches
-// (one wave per SIMD), two otherwise.
-constexpr int kTargetWorkgroupsPrefetch = 256;
-constexpr int kTargetWorkgroups = 512;
+// Workgroups of one attention call: one per CU (the register-prefetching
+// kernel of up to two row tiles holds one wave per SIMD; the many-row kernel
+// one workgroup of up to five waves per CU).
+constexpr int kTargetWorkgroups = 256;
 constexpr int kMaxSplits = 16;
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -230,8 +236,11 @@ __device__ __forceinline__ uint64_t map_mask(int ks, int slot, int entry) {
   return __builtin_amdgcn_ballot_w64(slot < ks && entry >= 0);
 }
 
+// Split kernel for one or two row tiles (up to 32 rows): K and V straight
+// into registers, every wave a strided subset of the split's units.
 template <int NT, int BS>
 __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
+  static_assert(NT <= 2, "three or more row tiles take attn_split_rows_kernel");
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
   const int lane = threadIdx.x & 63;
   const int g = lane >> 4;
@@ -312,35 +321,25 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
     process_unit<NT, BS>(cur, keep, partial, qb, m_run, l_run, acc, a.scale_log2);
   };
 
-  // With few row tiles the next unit's K/V loads are issued before the current
-  // unit is computed (one exposed memory latency per wave, not per unit); with
-  // many row tiles the registers go to the accumulators instead. Loads past the
-  // wave's last unit are placeholders on the local slot (cache-resident), so the
+  // The next unit's K/V loads are issued before the current unit is computed
+  // (one exposed memory latency per wave, not per unit). Loads past the wave's
+  // last unit are placeholders on the local slot (cache-resident), so the
   // compiler's wait counts stay exact.
-  constexpr bool kPrefetch = NT <= 2;
   auto settle = [&]() {  // the map entries and the context length are in
     asm volatile("" : "+v"(map_entry), "+v"(ctx_raw));
     vmask = map_mask(ks, map_slot, map_entry);
     local_len = ctx_blocks(ctx_raw, BS, a.NBmax).local_len;
   };
-  if (kPrefetch) {
-    load_unit<BS>(ub, unit(1), ks, pk, pv, slot_elems, g, i);
-    __builtin_amdgcn_sched_barrier(0);  // both units' loads are issued before the first wait
-    settle();
-    for (int t = 0; t < nt;) {
-      run(ua, t);
-      if (++t >= nt) break;
-      load_unit<BS>(ua, unit(t + 1), ks, pk, pv, slot_elems, g, i);
-      run(ub, t);
-      if (++t >= nt) break;
-      load_unit<BS>(ub, unit(t + 1), ks, pk, pv, slot_elems, g, i);
-    }
-  } else {
-    settle();
-    for (int t = 0; t < nt; ++t) {
-      if (t > 0) load_unit<BS>(ua, unit(t), ks, pk, pv, slot_elems, g, i);
-      run(ua, t);
-    }
+  load_unit<BS>(ub, unit(1), ks, pk, pv, slot_elems, g, i);
+  __builtin_amdgcn_sched_barrier(0);  // both units' loads are issued before the first wait
+  settle();
+  for (int t = 0; t < nt;) {
+    run(ua, t);
+    if (++t >= nt) break;
+    load_unit<BS>(ua, unit(t + 1), ks, pk, pv, slot_elems, g, i);
+    run(ub, t);
+    if (++t >= nt) break;
+    load_unit<BS>(ub, unit(t + 1), ks, pk, pv, slot_elems, g, i);
   }
   // row sums: add the partial sums of the four lanes of every row
 #pragma unroll
@@ -353,14 +352,12 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   // Each wave publishes its row maxima and sums; every lane then reads those of
   // all waves for its rows (all reads issued before any is used, no branch on
   // them), rescales its accumulators to the merged maximum and writes them to
-  // its slice (kSlices slices; with fewer slices than waves the other waves add
-  // into them in a second round); finally every thread sums the slices of a few
-  // (row, 4-dimension) positions, all their reads again issued at once.
+  // its slice; finally every thread sums the slices of a few (row, 4-dimension)
+  // positions, all their reads again issued at once.
   constexpr int kRows = NT * 16;
   constexpr int kPad = kHeadDim + 4;
-  constexpr int kSlices = NT <= 4 ? kW : 2;  // LDS: kSlices * kRows * kPad floats <= 160 KiB
   __shared__ float s_m[kW][kRows], s_l[kW][kRows], s_ml[2][kRows];
-  __shared__ __align__(16) float s_o[kSlices][kRows][kPad];
+  __shared__ __align__(16) float s_o[kW][kRows][kPad];
   if (g == 0) {
 #pragma unroll
     for (int v = 0; v < NT; ++v) {
@@ -393,19 +390,11 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
     }
   }
 #pragma unroll
-  for (int round = 0; round < kW / kSlices; ++round) {
-    if (wave / kSlices == round) {
-      const int sl = wave % kSlices;
+  for (int v = 0; v < NT; ++v)
 #pragma unroll
-      for (int v = 0; v < NT; ++v)
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) {
-          f32x4* dst = reinterpret_cast<f32x4*>(&s_o[sl][v * 16 + i][dt * 16 + 4 * g]);
-          *dst = round > 0 ? *dst + acc[v][dt] : acc[v][dt];
-        }
-    }
-    __syncthreads();
-  }
+    for (int dt = 0; dt < 8; ++dt)
+      *reinterpret_cast<f32x4*>(&s_o[wave][v * 16 + i][dt * 16 + 4 * g]) = acc[v][dt];
+  __syncthreads();
 
   const int nsplit = a.nsplit;
   const long long pbase = ((long long)rh * nsplit + split) * a.rows;
@@ -419,7 +408,7 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
     const int c4 = pos & 31;
     o[j] = *reinterpret_cast<const f32x4*>(&s_o[0][row][c4 * 4]);
 #pragma unroll
-    for (int sl = 1; sl < kSlices; ++sl) o[j] += *reinterpret_cast<const f32x4*>(&s_o[sl][row][c4 * 4]);
+    for (int sl = 1; sl < kW; ++sl) o[j] += *reinterpret_cast<const f32x4*>(&s_o[sl][row][c4 * 4]);
   }
 #pragma unroll
   for (int j = 0; j < kPer; ++j) {
@@ -440,54 +429,284 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
   }
 }
 
-// Merge of the NS splits: one workgroup per (row, request x KV head), one thread
-// per dimension; every thread issues its NS partial loads and the row's NS
-// (max, sum) pairs at once. Workgroup ids are dealt so that the head's id % 8,
-// which places its splits on one XCD, places its merge there too: the partials
-// are read from the L2 that holds them.
-template <int NS>
-__global__ __launch_bounds__(kHeadDim) void attn_merge_kernel(AttnArgs a) {
+// Split kernel for many row tiles (NT >= 3: G * T > 32 rows). A workgroup has
+// one wave per row tile; every wave attends its 16 rows to every unit of the
+// split, so the waves never merge softmax states and each writes its own rows.
+// Each unit's K and V cross HBM once: its 16 chunks (8 of K, 8 of V, 16 bytes
+// a lane, in the MFMA operand layout of load_unit) are loaded straight into
+// LDS, dealt round-robin to the waves, and every wave reads all 16 back as
+// conflict-free 16-byte LDS reads. A ring of kRowsStages units keeps
+// kRowsStages - 1 units in flight; one barrier per unit publishes a unit to
+// every wave and frees the stage of the one before.
+//
+// Measured on MI355X (16 requests x 8 KV heads x 72 rows, B = 32, 4,096
+// tokens per head, 268 MB): 81.7 us for the register kernel (every wave loads
+// the units of its own split range, five row tiles per wave), 63 to 66 us here
+// with the merge. Registers staged through VGPRs instead of direct-to-LDS
+// loads, two units ahead: 67 to 70 us; six stages instead of four, or two
+// workgroups per CU: no gain. The loads alone (no arithmetic) take 57 to 60
+// us against 48 us for a plain streaming read of the same bytes.
+constexpr int kRowsStages = 4;
+typedef u32x4 UnitLds[17][64];  // [chunk][lane]; chunk 16 takes the surplus loads
+
+template <int BS>
+__device__ __forceinline__ const uint16_t* chunk_src(int u, int j, int ks, const uint16_t* pk, const uint16_t* pv,
+                                                     long long slot_elems, int g, int i) {
+  // lane (g, i)'s 16 bytes of chunk j of unit u: j < 8 is K token tile tau = j / 4 at
+  // k-step st = j % 4, j >= 8 is V d-tile j - 8 (the addresses load_unit reads)
+  const bool real = u >= 0;
+  const int s0 = real ? (BS == 16 ? 2 * u : u) : ks;
+  const int s1raw = real ? (BS == 16 ? 2 * u + 1 : ks + 1) : ks + 1;
+  const int s1 = s1raw <= ks ? s1raw : ks;
+  if (j < 8) {
+    const int tau = j >> 2, st = j & 3;
+    const int tok = 8 * (i >> 2) + 4 * tau + (i & 3);
+    const uint16_t* k0 = pk + (long long)s0 * slot_elems;
+    const uint16_t* k1 = pk + (long long)s1 * slot_elems;
+    const uint16_t* src = BS == 16 ? ((tok < 16 ? k0 : k1) + (tok & 15) * kHeadDim + g * 8)
+                                   : (k0 + tok * kHeadDim + g * 8);
+    return src + st * 32;
+  }
+  const int dt = j - 8;
+  const uint16_t* v0 = pv + (long long)s0 * slot_elems;
+  const uint16_t* v1 = pv + (long long)s1 * slot_elems;
+  const uint16_t* vsrc = BS == 16 ? ((g < 2 ? v0 : v1) + (g & 1) * 8) : (v0 + 8 * g);
+  return vsrc + (long long)(dt * 16 + i) * BS;
+}
+
+// 16 bytes a lane from global memory straight into LDS (global_load_lds_dwordx4):
+// lane L's bytes land at lds_row + 16 L, lds_row being the same in every lane.
+// Written as inline assembly because the compiler, which cannot tell the ring's
+// stages apart once they are reused, would otherwise wait for every earlier
+// such load before each one (a full drain per unit); the waits are the
+// explicit vmcnt counts of the kernel instead. The "memory" clobber keeps LDS
+// reads and writes in program order around it, and M0 (the LDS base operand
+// of the load) is restored after it.
+__device__ __forceinline__ void lds_dma16(const void* gsrc, void* lds_row) {
+  const uint32_t lds =
+      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds_row);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gsrc), "s"(lds)
+      : "memory");
+}
+
+// s_waitcnt vmcnt(N) alone (expcnt and lgkmcnt left at their maxima)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// f(std::integral_constant<int, 0>{}), ..., f(std::integral_constant<int, N - 1>{})
+template <typename F, int... S>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, S...>) {
+  (f(std::integral_constant<int, S>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+template <int NT, int BS>
+__global__ __launch_bounds__(NT * 64) void attn_split_rows_kernel(AttnArgs a) {
+  static_assert(kRowsStages == 4, "one LDS variable per stage below");
+  constexpr int kPer = (16 + NT - 1) / NT;  // chunk loads per wave and unit
+  // One LDS variable per stage, always named with a compile-time stage, so the
+  // compiler sees each read of a stage apart from the other stages' loads.
+  // Every wave issues kPer loads a unit (the surplus ones re-read chunk 0 into
+  // row 16), so that one vmcnt count fits every wave.
+  __shared__ __align__(16) UnitLds s_st0;
+  __shared__ __align__(16) UnitLds s_st1;
+  __shared__ __align__(16) UnitLds s_st2;
+  __shared__ __align__(16) UnitLds s_st3;
+  auto stage_buf = [&](auto S) __attribute__((always_inline)) -> UnitLds& {
+    constexpr int k = decltype(S)::value;
+    if constexpr (k == 0) return s_st0;
+    else if constexpr (k == 1) return s_st1;
+    else if constexpr (k == 2) return s_st2;
+    else return s_st3;
+  };
+  const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // this wave's row tile
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4;
+  const int i = lane & 15;
   const int nrh = a.R * a.Hkv;
+  int rh, split;
+  if (!map_workgroup(blockIdx.x, nrh, a.nsplit, rh, split)) return;
+  const int r = rh / a.Hkv;
+  const int h = rh - r * a.Hkv;
+  const int ks = a.k_slots;
+  const long long slot_elems = (long long)a.Hkv * BS * kHeadDim;
+  const long long head_off = (long long)h * BS * kHeadDim;
+  const uint16_t* pk = a.pool_k + (long long)r * (ks + 1) * slot_elems + head_off;
+  const uint16_t* pv = a.pool_v + (long long)r * (ks + 1) * slot_elems + head_off;
+  const int32_t* smap = a.slot_map + (long long)rh * ks;
+  const int u_begin = split * a.units_per_split;
+  const int u_end = min(a.n_units, u_begin + a.units_per_split);
+  const int nt = u_end > u_begin ? u_end - u_begin : 0;  // units of this workgroup, in order
+  auto unit = [&](int t) __attribute__((always_inline)) { return t < nt ? u_begin + t : -1; };
+
+  // this wave's chunk loads of unit t into stage S (past the last unit: the placeholder slot)
+  auto issue = [&](int t, auto S) __attribute__((always_inline)) {
+    UnitLds& buf = stage_buf(S);
+    const int u = unit(t);
+#pragma unroll
+    for (int c = 0; c < kPer; ++c) {
+      const int j = v + c * NT;
+      lds_dma16(chunk_src<BS>(u, j < 16 ? j : 0, ks, pk, pv, slot_elems, g, i), &buf[j < 16 ? j : 16][0]);
+    }
+  };
+  // validity mask of units t .. t + kChunkU - 1 (lane l: map entry of slot l % 2 of
+  // unit t + l / 2 at B = 16, of unit t + l at B = 32)
+  constexpr int kChunkU = BS == 16 ? 32 : 64;
+  auto mask_slot = [&](int t) __attribute__((always_inline)) {
+    const int jj = BS == 16 ? lane >> 1 : lane;
+    return BS == 16 ? 2 * (u_begin + t + jj) + (lane & 1) : u_begin + t + jj;
+  };
+  const int slot0 = mask_slot(0);
+  const int entry0 = map_load(smap, ks, slot0, a.ctx_len + r);
+  static_for<kRowsStages - 1>([&](auto S) __attribute__((always_inline)) { issue(decltype(S)::value, S); });
+
+  // Q^T operand of row tile v
+  bf16x8 qb[1][4];
+  const int row = v * 16 + i;
+  if (row < a.rows) {
+    const int tq = row / a.G;
+    const int qh = h * a.G + (row - tq * a.G);
+    const uint16_t* qrow = a.q + (((long long)r * a.T + tq) * a.Hq + qh) * kHeadDim;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) qb[0][st] = as_bf16x8(ldg16(qrow + st * 32 + g * 8));
+  } else {
+#pragma unroll
+    for (int st = 0; st < 4; ++st) qb[0][st] = as_bf16x8(u32x4{0, 0, 0, 0});
+  }
+  const Ctx c = ctx_blocks(a.ctx_len[r], BS, a.NBmax);
+  const int local_len = c.local_len;
+
+  float m_run[1] = {-INFINITY}, l_run[1] = {0.f};
+  f32x4 acc[1][8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) acc[0][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint64_t vmask = map_mask(ks, slot0, entry0);
+
+  // unit t sits in stage t % kRowsStages
+  auto step = [&](int t, auto S) __attribute__((always_inline)) {
+    constexpr int k = decltype(S)::value;
+    if (t > 0 && (t & (kChunkU - 1)) == 0) {
+      const int slot = mask_slot(t);
+      vmask = map_mask(ks, slot, map_load(smap, ks, slot, a.ctx_len + r));
+    }
+    // this wave's loads of unit t are done (those of the kRowsStages - 2 later units may
+    // still fly); the barrier publishes every wave's loads of unit t and tells that the
+    // stage of unit t - 1 is no longer read
+    wait_vmcnt<kPer * (kRowsStages - 2)>();
+    __syncthreads();
+    issue(t + kRowsStages - 1, std::integral_constant<int, (k + kRowsStages - 1) % kRowsStages>{});
+    const UnitLds& buf = stage_buf(S);
+    UnitRegs cur;
+#pragma unroll
+    for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+      for (int st = 0; st < 4; ++st) cur.k[tau][st] = buf[tau * 4 + st][lane];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) cur.v[dt] = buf[8 + dt][lane];
+    int n0, n1;
+    const int bit = BS == 16 ? 2 * (t & (kChunkU - 1)) : (t & (kChunkU - 1));
+    unit_counts<BS>(unit(t), ks, local_len, vmask, bit, n0, n1);
+    const int keep = lane_keep<BS>(n0, n1, g);
+    const bool partial = __builtin_amdgcn_ballot_w64(keep < 8) != 0;
+    if (partial) mask_unit_v(cur, keep);
+    process_unit<1, BS>(cur, keep, partial, qb, m_run, l_run, acc, a.scale_log2);
+  };
+  int t = 0;
+  for (; t + kRowsStages <= nt; t += kRowsStages)
+    static_for<kRowsStages>([&](auto S) __attribute__((always_inline)) { step(t + decltype(S)::value, S); });
+  static_for<kRowsStages - 1>([&](auto S) __attribute__((always_inline)) {
+    if (t + decltype(S)::value < nt) step(t + decltype(S)::value, S);
+  });
+  wait_vmcnt<0>();  // the placeholder loads past the last unit land before the workgroup ends
+  float L = l_run[0] + __shfl_xor(l_run[0], 16);
+  L += __shfl_xor(L, 32);
+  const float M = m_run[0];
+  if (row >= a.rows) return;
+  if (a.nsplit == 1) {
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) write_output(a, r, h, row, dt * 4 + g, acc[0][dt], M, L);
+    return;
+  }
+  const long long pr = ((long long)rh * a.nsplit + split) * a.rows + row;
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<f32x4*>(a.part_o + pr * kHeadDim + dt * 16 + 4 * g) = acc[0][dt];
+  if (g == 0) *reinterpret_cast<float2*>(a.part_ml + pr * 2) = make_float2(M, L);
+}
+
+// Merge of the NS splits: a workgroup takes kMergeRows rows of one (request,
+// KV head), 32 threads a row, each thread 4 dimensions; every thread issues its
+// NS partial loads (16 bytes each) and the row's NS (max, sum) pairs at once.
+// Workgroup ids are dealt so that the head's id % 8, which places its splits on
+// one XCD, places its merge there too: the partials are read from the L2 that
+// holds them.
+constexpr int kMergeRows = 8;
+
+template <int NS>
+__global__ __launch_bounds__(kMergeRows * 32) void attn_merge_kernel(AttnArgs a) {
+  const int nrh = a.R * a.Hkv;
+  const int groups = (a.rows + kMergeRows - 1) / kMergeRows;
   const int wg = blockIdx.x;
   const int local = wg >> 3;
-  const int rh_local = local / a.rows;
-  const int row = local - rh_local * a.rows;
+  const int rh_local = local / groups;
+  const int grp = local - rh_local * groups;
   const int rh = rh_local * 8 + (wg & 7);
-  if (rh >= nrh) return;
-  const int d = threadIdx.x;
+  const int row = grp * kMergeRows + (threadIdx.x >> 5);
+  if (rh >= nrh || row >= a.rows) return;
+  const int c4 = threadIdx.x & 31;
   const int r = rh / a.Hkv;
   const int h = rh - r * a.Hkv;
   const long long base = (long long)rh * NS * a.rows + row;
-  float ms[NS], ls[NS], os[NS];
+  float2 ml[NS];
+  f32x4 os[NS];
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
     const long long idx = base + (long long)s * a.rows;
-    ms[s] = a.part_ml[idx * 2];
-    ls[s] = a.part_ml[idx * 2 + 1];
-    os[s] = a.part_o[idx * kHeadDim + d];
+    ml[s] = *reinterpret_cast<const float2*>(a.part_ml + idx * 2);
+    os[s] = *reinterpret_cast<const f32x4*>(a.part_o + idx * kHeadDim + c4 * 4);
   }
-  float M = ms[0];
+  float M = ml[0].x;
 #pragma unroll
-  for (int s = 1; s < NS; ++s) M = fmaxf(M, ms[s]);
+  for (int s = 1; s < NS; ++s) M = fmaxf(M, ml[s].x);
   // a split with no attended token (max -inf) weighs 0; with none at all, L = 0
-  float L = 0.f, o = 0.f;
+  float L = 0.f;
+  f32x4 o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
-    const float f = ms[s] == -INFINITY ? 0.f : fast_exp2(ms[s] - M);
-    L += ls[s] * f;
-    o += os[s] * f;
+    const float f = ml[s].x == -INFINITY ? 0.f : fast_exp2(ml[s].x - M);
+    L += ml[s].y * f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] += os[s][e] * f;
   }
-  const float res = L > 0.f ? o / L : 0.f;
+  float res[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) res[e] = L > 0.f ? o[e] / L : 0.f;
   const int t = row / a.G;
   const int qh = h * a.G + (row - t * a.G);
   const long long orow = ((long long)r * a.T + t) * a.Hq + qh;
-  a.out[orow * kHeadDim + d] = (uint16_t)f32_to_bf16_bits(res);
-  if (d == 0 && a.lse) a.lse[orow] = L > 0.f ? (M + __log2f(L)) * 0.69314718055994531f : -INFINITY;
+  const uint32_t w0 = f32_to_bf16_bits(res[0]) | (f32_to_bf16_bits(res[1]) << 16);
+  const uint32_t w1 = f32_to_bf16_bits(res[2]) | (f32_to_bf16_bits(res[3]) << 16);
+  *reinterpret_cast<uint2*>(a.out + orow * kHeadDim + c4 * 4) = make_uint2(w0, w1);
+  if (c4 == 0 && a.lse) a.lse[orow] = L > 0.f ? (M + __log2f(L)) * 0.69314718055994531f : -INFINITY;
 }
 
 template <int NS>
 void launch_merge_ns(const AttnArgs& a, hipStream_t s, const LaunchTiming& t, int nrh8) {
-  launch_kernel(attn_merge_kernel<NS>, dim3((unsigned)(nrh8 * a.rows)), dim3(kHeadDim), s, t, a);
+  const int groups = (a.rows + kMergeRows - 1) / kMergeRows;
+  launch_kernel(attn_merge_kernel<NS>, dim3((unsigned)(nrh8 * groups)), dim3(kMergeRows * 32), s, t, a);
 }
 
 void launch_merge(const AttnArgs& a, hipStream_t s, const LaunchTiming& t, int nrh8) {
@@ -516,8 +735,12 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t s, const LaunchTiming& t) {
   const int nrh8 = (nrh + 7) / 8 * 8;
   const bool merge = a.nsplit > 1;
   // timed as one span: from the split kernel's start to the merge kernel's end
-  launch_kernel(attn_split_kernel<NT, BS>, dim3((unsigned)(nrh8 * a.nsplit)), dim3(kW * 64), s,
-                LaunchTiming{t.start, merge ? nullptr : t.stop}, a);
+  if constexpr (NT >= 3)
+    launch_kernel(attn_split_rows_kernel<NT, BS>, dim3((unsigned)(nrh8 * a.nsplit)), dim3(NT * 64), s,
+                  LaunchTiming{t.start, merge ? nullptr : t.stop}, a);
+  else
+    launch_kernel(attn_split_kernel<NT, BS>, dim3((unsigned)(nrh8 * a.nsplit)), dim3(kW * 64), s,
+                  LaunchTiming{t.start, merge ? nullptr : t.stop}, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !merge) return e;
   launch_merge(a, s, LaunchTiming{nullptr, t.stop}, nrh8);
@@ -544,8 +767,7 @@ AttnPlan attn_plan(int R, int Hq, int Hkv, int T, int B, int k_slots) {
   p.rows = G * T;
   p.n_units = B == 16 ? (k_slots + 2) / 2 : k_slots + 1;
   const long long nrh = (long long)R * Hkv;
-  const int target = (p.rows + 15) / 16 <= 2 ? kTargetWorkgroupsPrefetch : kTargetWorkgroups;
-  long long want = (target + nrh - 1) / (nrh > 0 ? nrh : 1);
+  long long want = (kTargetWorkgroups + nrh - 1) / (nrh > 0 ? nrh : 1);
   const long long most = (p.n_units + kW - 1) / kW;  // at least one unit per wave
   if (want > most) want = most;
   if (want > kMaxSplits) want = kMaxSplits;

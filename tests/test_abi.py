@@ -48,7 +48,7 @@ def test_exports_match_header(lib):
 
 
 def test_abi_version(lib):
-    assert lib.oasis_abi_version() == 6
+    assert lib.oasis_abi_version() == 7
 
 
 def test_argument_checks_without_gpu(lib):
@@ -165,10 +165,10 @@ def test_noalloc_attention_checks_without_gpu(lib):
     assert L.oasis_sparse_decode_attn_noalloc(ctypes.byref(ok), None, 5, None, None, None, 128, None, 0.1, None,
                                               None, None) == 1
     assert "is NULL" in lib.oasis_last_error()
-    # 504 pairs x 2 splits x 80 rows x 130 floats = 41.9 MB of partials > the 32 MiB scratch
-    big = lib.dims(63, 128, 8, 128, 16, 8192)
+    # 255 pairs (G = 16: 80 rows) x 2 splits x 80 rows x 130 floats = 21.2 MB of partials > the 16 MiB scratch
+    big = lib.dims(255, 16, 1, 128, 16, 8192)
     need = lib.oasis_attn_workspace_bytes(big, 5, 128)
-    assert need == 504 * 2 * 80 * 130 * 4 and need > lib._lib.NOALLOC_SCRATCH_BYTES
+    assert need == 255 * 2 * 80 * 130 * 4 and need > lib._lib.NOALLOC_SCRATCH_BYTES
     assert L.oasis_sparse_decode_attn_noalloc(ctypes.byref(big), None, 5, None, None, None, 128, None, 0.1, None,
                                               None, None) == 2
     assert "scratch" in lib.oasis_last_error()

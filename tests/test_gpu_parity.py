@@ -414,6 +414,11 @@ ATTN_CASES = [
     (8, 2, 16, 2, 5, 32, 33, [1000, 64], 0.25),
     (9, 2, 64, 8, 7, 16, 50, [4000, 777], 0.2),          # 56 rows: four row tiles
     (10, 2, 48, 8, 6, 32, 20, [3000, 100], 0.3),         # G = 6: 36 rows, three row tiles, B = 32
+    (11, 2, 40, 8, 8, 16, 60, [4000, 950], 0.2),         # G = 5: 40 rows, three row tiles, B = 16
+    (12, 2, 64, 8, 7, 32, 40, [2600, 1000], 0.2),        # 56 rows, four row tiles, B = 32
+    (13, 2, 64, 8, 9, 16, 70, [3000, 1111], 0.3),        # 72 rows, five row tiles, B = 16
+    # 256 (request, KV head) pairs: one split each, the many-row kernel writes the outputs itself
+    (14, 32, 64, 8, 9, 32, 6, [6 * 32 + 5 + 3 * r for r in range(32)], 0.2),
 ]
 
 

@@ -43,32 +43,40 @@ import time
 import numpy as np
 
 # The pipelined step keeps three streams busy at once (foreground, prediction,
-# transfer). With HIP's default of 4 hardware queues per process the runtime
-# can place two of them on one queue, where each serializes behind the other's
-# waits (measured: about 1 process in 6 ran 2.5x slower). More queues give every
-# stream its own; this must be set before HIP initializes.
-os.environ.setdefault("GPU_MAX_HW_QUEUES", "16")
+# transfer). A kernel trace at HIP's default of 4 hardware queues per process
+# shows them on three distinct queues, and the step rate is the same at 4 and
+# at 16 queues (c4: 10,490 / 10,463 / 10,492 against 10,524 / 10,450 / 10,514
+# steps/s, three processes each); the run takes whatever the environment sets
+# and records it.
+HW_QUEUES = os.environ.get("GPU_MAX_HW_QUEUES")
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
-TRAFFIC_NOTE = os.path.join(ROOT, "profiles", "score_kernel_c4_hbm_traffic.md")
+TRAFFIC_NOTE = os.path.join(ROOT, "profiles", "c4_score_attention_hbm_traffic.md")
 
 
-def measured_traffic():
-    """HBM bytes per scorer launch from the committed FETCH_SIZE / WRITE_SIZE passes, or None
-    if they were taken on a different score.hip (or are missing)."""
+def measured_traffic(kind):
+    """HBM bytes per launch ("score": the scorer; "attention": split + merge of one call) from the
+    committed FETCH_SIZE / WRITE_SIZE passes, or None if the sources they name have changed since
+    (their sha256 differs) or the note is missing."""
     import hashlib
     import re
+    key = {"score": ("score_kernel_traffic_bytes", "score_sources_sha256"),
+           "attention": ("attention_traffic_bytes", "attn_sources_sha256")}[kind]
+    files = {"score": ("score.hip", "score_core.h", "oasis_internal.h"),
+             "attention": ("attn.hip", "oasis_internal.h")}[kind]
     try:
         note = open(TRAFFIC_NOTE).read()
-        src = open(os.path.join(ROOT, "paper_2608_08097_amd", "csrc", "score.hip"), "rb").read()
+        h = hashlib.sha256()
+        for f in files:
+            h.update(open(os.path.join(ROOT, "paper_2608_08097_amd", "csrc", f), "rb").read())
     except OSError:
         return None
-    m = re.search(r"score_kernel_traffic_bytes=(\d+) score_hip_sha256=([0-9a-f]{64})", note)
-    if not m or m.group(2) != hashlib.sha256(src).hexdigest():
+    m = re.search(key[0] + r"=(\d+) " + key[1] + r"=([0-9a-f]{64})", note)
+    if not m or m.group(2) != h.hexdigest():
         return None
     return int(m.group(1))
 
@@ -462,16 +470,18 @@ def main():
             "fetch_ratio": args.fetch_ratio if fetch_cap < K else "all", "fetch_cap": fetch_cap,
             "parallelism": "single GPU", "plan_stream": "prediction" if plan_on_prediction(args) else "transfer",
             "fused_prediction": args.fused_prediction,
+            "gpu_max_hw_queues": HW_QUEUES if HW_QUEUES is not None else "unset (HIP default, 4)",
         },
         "roofline": {
             "bound": "hbm", "kernel": "score_kernel (oasis_score_blocks)",
             "achieved": round(score_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(score_gbs / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic() if args.workload == "c4" else None,
+            "traffic": measured_traffic("score") if args.workload == "c4" else None,
             "algorithmic_bytes": score_bytes, "avg_us": round(iso["score"], 2),
             "timing": "64 back-to-back launches over the rotating layer states, one event pair",
         },
         "attention": {"avg_us": round(iso["attn"], 2), "algorithmic_bytes": attn_bytes,
+                      "traffic": measured_traffic("attention") if args.workload == "c4" else None,
                       "achieved_GBs": round(attn_gbs, 1), "frac": round(attn_gbs / HBM_PEAK_GBS, 4),
                       "frac_of_measured_read": round(attn_gbs / peaks["hbm_read_GBs"], 4)},
         "score_frac_of_measured_read": round(score_gbs / peaks["hbm_read_GBs"], 4),
@@ -606,7 +616,8 @@ def run_reasoning(args, P, torch, DecodePath):
                                f"{args.budget} (K={K}), fetch cap {fetch_cap}, {S} steps of one token",
                    "global_batch": c.num_reqs, "layers": NL, "fetch_cap": fetch_cap,
                    "plan_stream": "prediction" if plan_on_prediction(args) else "transfer",
-                   "fused_prediction": args.fused_prediction},
+                   "fused_prediction": args.fused_prediction,
+                   "gpu_max_hw_queues": HW_QUEUES if HW_QUEUES is not None else "unset (HIP default, 4)"},
         "tokens_per_s": round(c.num_reqs * S / elapsed, 1),
         "decode_step_ms_all_layers": round(t_step_us / 1e3, 3),
         "prefetch_rate": {"delta_prefetch_us": round(delta, 2), "t_pred_us": round(prof["score"] + prof["topk"], 2),

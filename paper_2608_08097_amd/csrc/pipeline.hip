@@ -20,7 +20,7 @@
 
 namespace {
 constexpr int kFlagStride = 64;  // uint32 per counter (256 bytes)
-constexpr int kQ = 0, kPred = 1, kAttn = 2, kJoinPred = 3, kJoinXfer = 4, kStaged0 = 5;  // counter slots
+constexpr int kQ = 0, kPred = 1, kJoinPred = 2, kJoinXfer = 3, kStaged0 = 4;  // counter slots
 constexpr uint32_t kWrapGuard = 1u << 30;
 constexpr int kProfKinds = 4;  // attention (split + merge), scoring, top-K, staging
 // (request, KV head) pairs from which OASIS_FUSED_PREDICTION_AUTO scores and
@@ -372,13 +372,15 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   const int sl = kStaged0 + layer;
   // foreground: this layer's previous transfer must have landed before its attention
   if (p->staged[layer]) HIP_TRY(wait_for(p, fg, sl, p->staged[layer]), fn);
-  // q and ctx_len are ready on the foreground; past the wait above this also
-  // means the previous transfer has finished reading sel and scores
-  HIP_TRY(signal_next(p, fg, kQ, &cnt[kQ]), fn);
-  HIP_TRY(wait_for(p, p->pred, kQ, cnt[kQ]), fn);
   if (growing) HIP_TRY(oasis::launch_stage(la, fg), fn);
   HIP_TRY(oasis::launch_attn(aa, fg, prof_timing(p, 0)), fn);
-  HIP_TRY(signal_next(p, fg, kAttn, &cnt[kAttn]), fn);
+  // One edge from the foreground, after the attention: q and ctx_len are
+  // ready; past the wait above, the previous transfer has finished reading sel
+  // and scores (which the prediction rewrites); and the attention is done with
+  // the pool slots this step's gather overwrites (the transfer is ordered
+  // behind the prediction, which is ordered behind this).
+  HIP_TRY(signal_next(p, fg, kQ, &cnt[kQ]), fn);
+  HIP_TRY(wait_for(p, p->pred, kQ, cnt[kQ]), fn);
   if (prev_ctx_len) HIP_TRY(oasis::launch_summaries(ua, p->pred), fn);
   // one workgroup per (request, KV head) scores and selects (and plans) when
   // the rows are many and short enough to fill the chip that way
@@ -401,7 +403,6 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   }
   HIP_TRY(signal_next(p, p->pred, kPred, &cnt[kPred]), fn);
   HIP_TRY(wait_for(p, p->xfer, kPred, cnt[kPred]), fn);
-  HIP_TRY(wait_for(p, p->xfer, kAttn, cnt[kAttn]), fn);  // the gather overwrites slots the attention reads
   HIP_TRY(oasis::launch_stage(ga, p->xfer, prof_timing(p, 3)), fn);
   HIP_TRY(signal_next(p, p->xfer, sl, &p->staged[layer]), fn);
   if (p->prof_ev && p->prof_n < p->prof_cap) ++p->prof_n;

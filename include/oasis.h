@@ -477,6 +477,14 @@ OASIS_API oasis_status oasis_pipeline_profile_begin(oasis_pipeline* pipeline, in
 OASIS_API oasis_status oasis_pipeline_profile_end(oasis_pipeline* pipeline, float* avg_us, float* step_us,
                                                   int32_t* steps);
 
+/* Synchronize the device, then report whether any transfer of this pipeline
+ * gave up waiting for its prediction. The staging kernel of a step waits for
+ * the step's prediction itself, polling the counter the prediction stream
+ * raises, for a few seconds at most; past that it marks a fault and proceeds (its
+ * results are then undefined) instead of holding the GPU. OASIS_OK when no
+ * fault was marked, OASIS_ERR_HIP when one was (or a HIP call failed). */
+OASIS_API oasis_status oasis_pipeline_check(oasis_pipeline* pipeline);
+
 /* Synchronize the device, then release the counters (and owned streams). NULL is a no-op. */
 OASIS_API void oasis_pipeline_destroy(oasis_pipeline* pipeline);
 

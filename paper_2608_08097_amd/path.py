@@ -210,13 +210,21 @@ class DecodePath:
         (with ``per_step``, also each step's four durations as a [steps, 4] array)."""
         return L.oasis_pipeline_profile_end(self._pipe, per_step)
 
+    def check(self):
+        """Synchronize the device and raise if a pipelined transfer gave up waiting for its prediction."""
+        if self._pipe is not None:
+            L.oasis_pipeline_check(self._pipe)
+
     def close(self):
-        """Wait for the background streams and release the native issuer."""
+        """Wait for the background streams, check the native issuer's transfers and release it."""
         if self._pipe is not None:
             self.side.synchronize()
             self.xfer.synchronize()
-            L.oasis_pipeline_destroy(self._pipe)
-            self._pipe = None
+            try:
+                L.oasis_pipeline_check(self._pipe)
+            finally:
+                L.oasis_pipeline_destroy(self._pipe)
+                self._pipe = None
 
     def __del__(self):
         try:

@@ -480,10 +480,18 @@ OASIS_API oasis_status oasis_pipeline_profile_end(oasis_pipeline* pipeline, floa
 /* Synchronize the device, then report whether any transfer of this pipeline
  * gave up waiting for its prediction. The staging kernel of a step waits for
  * the step's prediction itself, polling the counter the prediction stream
- * raises, for a few seconds at most; past that it marks a fault and proceeds (its
+ * raises, for a bounded time (oasis_pipeline_set_wait_limit; a few seconds by
+ * default); past that it marks a fault and proceeds (its
  * results are then undefined) instead of holding the GPU. OASIS_OK when no
  * fault was marked, OASIS_ERR_HIP when one was (or a HIP call failed). */
 OASIS_API oasis_status oasis_pipeline_check(oasis_pipeline* pipeline);
+
+/* Bound of the staging kernel's wait for its prediction, in polls (each about
+ * a microsecond; default 2^21, a few seconds), from the next step on. A smaller
+ * bound reports a stalled prediction sooner; a step whose prediction is merely
+ * slower than the bound then marks a fault too. Errors: INVALID_ARG for a NULL
+ * pipeline or polls = 0. */
+OASIS_API oasis_status oasis_pipeline_set_wait_limit(oasis_pipeline* pipeline, uint32_t polls);
 
 /* Synchronize the device, then release the counters (and owned streams). NULL is a no-op. */
 OASIS_API void oasis_pipeline_destroy(oasis_pipeline* pipeline);

@@ -28,7 +28,7 @@ EXPORTS = (
     "oasis_union_selection",
     "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_set_local_source",
     "oasis_pipeline_set_plan_stream", "oasis_pipeline_set_fused_prediction", "oasis_pipeline_step",
-    "oasis_pipeline_join", "oasis_pipeline_check",
+    "oasis_pipeline_join", "oasis_pipeline_check", "oasis_pipeline_set_wait_limit",
     "oasis_pipeline_destroy", "oasis_pipeline_profile_begin", "oasis_pipeline_profile_end",
 )
 
@@ -126,6 +126,8 @@ def lib() -> ctypes.CDLL:
         L.oasis_pipeline_join.argtypes = [_P, _P]
         L.oasis_pipeline_check.restype = _I32
         L.oasis_pipeline_check.argtypes = [_P]
+        L.oasis_pipeline_set_wait_limit.restype = _I32
+        L.oasis_pipeline_set_wait_limit.argtypes = [_P, ctypes.c_uint32]
         L.oasis_pipeline_destroy.restype = None
         L.oasis_pipeline_destroy.argtypes = [_P]
         L.oasis_pipeline_profile_begin.restype = _I32
@@ -475,6 +477,11 @@ def oasis_pipeline_join(handle: int, stream=None) -> None:
 def oasis_pipeline_check(handle: int) -> None:
     """Synchronize the device; raise if a transfer of the pipeline gave up waiting for its prediction."""
     _check("oasis_pipeline_check", lib().oasis_pipeline_check(handle))
+
+
+def oasis_pipeline_set_wait_limit(handle: int, polls: int) -> None:
+    """Bound (in polls, about 1 us each) of the staging kernel's wait for its prediction."""
+    _check("oasis_pipeline_set_wait_limit", lib().oasis_pipeline_set_wait_limit(handle, int(polls)))
 
 
 def oasis_pipeline_destroy(handle: int | None) -> None:

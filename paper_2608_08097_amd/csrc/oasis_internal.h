@@ -171,14 +171,16 @@ struct StageArgs {
   int32_t* ws;              // stage_ws_ints(R * Hkv, k) ints (modes 1 and 2)
   // When wait_flag is set, the staging kernel first waits until *wait_flag >=
   // wait_value (a counter that another stream's work raises): one thread of
-  // each workgroup polls it, for a bounded time (kStageWaitSpins sleeps); past
-  // that the workgroup stores 1 to *wait_fault and goes on.
+  // each workgroup polls it, at most wait_polls times; past that the
+  // workgroup stores 1 to *wait_fault and goes on.
   const uint32_t* wait_flag;
   uint32_t wait_value;
   uint32_t* wait_fault;
+  uint32_t wait_polls;
 };
-// polls of the staging kernel's counter wait before it gives up: each is a
-// 128-clock sleep and an uncached load (about a microsecond), a few seconds in all
+// default bound of the staging kernel's counter wait in the pipeline: each poll
+// is a 128-clock sleep and an uncached load (about a microsecond), a few
+// seconds in all
 constexpr uint32_t kStageWaitSpins = 1u << 21;
 constexpr int kStagePlanCopy = 0, kStagePlanOnly = 1, kStageCopyOnly = 2;
 // Plan workspace: [nrh][k] map rows, [nrh][k] stamp rows, [nrh][k][2] entries (slot, page), [nrh] counts.

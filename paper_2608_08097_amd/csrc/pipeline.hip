@@ -53,6 +53,7 @@ struct oasis_pipeline {
   int32_t** plan_ws;            // [max_layers]: device staging-plan workspace of each layer (set_layer)
   bool plan_on_pred;            // OASIS_PLAN_ON_PREDICTION
   int32_t fused_pred;           // OASIS_FUSED_PREDICTION_*: score and top-K (+ plan) in one kernel
+  uint32_t wait_polls;          // bound of the staging kernel's wait for its prediction
   // optional profile: timing events around each kernel of the next prof_cap steps
   int32_t prof_cap, prof_n;
   hipEvent_t* prof_ev;          // [prof_cap][kProfKinds][2]
@@ -221,6 +222,7 @@ oasis_status oasis_pipeline_create(const oasis_dims* dims, int32_t num_q_tokens,
   p->local_num_pages = num_pages;
   p->local_block_table = host_block_table;
   p->max_layers = max_layers;
+  p->wait_polls = oasis::kStageWaitSpins;
   p->layers = new (std::nothrow) oasis_layer_buffers[max_layers]();
   p->staged = new (std::nothrow) uint32_t[max_layers]();
   p->is_set = new (std::nothrow) bool[max_layers]();
@@ -313,6 +315,14 @@ oasis_status oasis_pipeline_set_fused_prediction(oasis_pipeline* p, int32_t mode
   if (mode != OASIS_FUSED_PREDICTION_AUTO && mode != OASIS_FUSED_PREDICTION_OFF && mode != OASIS_FUSED_PREDICTION_ON)
     return fail(OASIS_ERR_INVALID_ARG, "%s: mode = %d is not an OASIS_FUSED_PREDICTION_* value", fn, mode);
   p->fused_pred = mode;
+  return ok();
+}
+
+oasis_status oasis_pipeline_set_wait_limit(oasis_pipeline* p, uint32_t polls) {
+  static const char* fn = "oasis_pipeline_set_wait_limit";
+  if (!p) return fail(OASIS_ERR_INVALID_ARG, "%s: pipeline is NULL", fn);
+  if (polls == 0) return fail(OASIS_ERR_INVALID_ARG, "%s: polls must be at least 1", fn);
+  p->wait_polls = polls;
   return ok();
 }
 
@@ -411,6 +421,7 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   ga.wait_flag = slot(p, kPred);
   ga.wait_value = cnt[kPred];
   ga.wait_fault = fault_word(p);
+  ga.wait_polls = p->wait_polls;
   HIP_TRY(oasis::launch_stage(ga, p->xfer, prof_timing(p, 3)), fn);
   HIP_TRY(signal_next(p, p->xfer, sl, &p->staged[layer]), fn);
   if (p->prof_ev && p->prof_n < p->prof_cap) ++p->prof_n;

@@ -540,14 +540,15 @@ __device__ __forceinline__ void copy_entries(const StageArgs& a, int n, const in
 // saves the transfer stream a dispatch per step. Thread 0 polls with relaxed
 // agent-scope loads; the barrier holds the other waves; the acquire fence then
 // orders every later read after the producer's writes, which its kernel's end
-// released before the counter was raised. The poll is bounded: a counter that
-// is never raised costs a few seconds and a fault mark, not a hang.
+// released before the counter was raised. The poll is bounded (wait_polls, a
+// few seconds by default): a counter that is never raised costs that time and
+// a fault mark, not a hang.
 __device__ __forceinline__ void stage_wait(const StageArgs& a) {
   if (!a.wait_flag) return;
   if (threadIdx.x == 0) {
     uint32_t n = 0;
     while (__hip_atomic_load(a.wait_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < a.wait_value) {
-      if (++n == kStageWaitSpins) {
+      if (++n >= a.wait_polls) {
         __hip_atomic_store(a.wait_fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
       }

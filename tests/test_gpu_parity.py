@@ -6,6 +6,7 @@ the block size or of the 16-block scoring tile, budgets larger than the
 candidate count, empty and one-token contexts).
 """
 import math
+import time
 
 import numpy as np
 import pytest
@@ -627,6 +628,67 @@ def test_pipelined_layers_native(plan_pred, fused):
         assert np.array_equal(host_bits(st.pool_k), r["pk"]), l
         assert np.array_equal(pool_v_to_htd(host_bits(st.pool_v)), r["pv"]), l
     path.close()
+
+
+def _independent_stream_pair(tries: int = 8):
+    """Two streams on different hardware queues: a bounded sleep kernel on the first must not hold
+    up a small kernel on the second. HIP maps a process's streams onto a few hardware queues, so two
+    pool streams may share one (then the second waits behind the first)."""
+    cands = [torch.cuda.Stream() for _ in range(tries)]
+    x = torch.zeros(1, device="cuda")
+    for i in range(tries):
+        for j in range(tries):
+            if i == j:
+                continue
+            torch.cuda.synchronize()
+            with torch.cuda.stream(cands[i]):
+                torch.cuda._sleep(100_000_000)  # tens of ms
+            t0 = time.perf_counter()
+            with torch.cuda.stream(cands[j]):
+                x.add_(1)
+            cands[j].synchronize()
+            quick = time.perf_counter() - t0 < 0.005
+            cands[i].synchronize()
+            if quick:
+                return cands[i], cands[j]
+    return None
+
+
+def test_pipeline_wait_fault_reported():
+    """Failure path of the transfer's in-kernel wait for its prediction: with the bound set to 64
+    polls and a stalled prediction stream (a bounded torch sleep kernel queued ahead of it), the
+    staging kernel gives up, every kernel still ends, and oasis_pipeline_check reports the fault;
+    a normal step before it reports none. The prediction and transfer streams are chosen on
+    different hardware queues, so that the transfer's kernel runs while the prediction sleeps."""
+    pair = _independent_stream_pair()
+    assert pair is not None, "no two of 8 streams run independently"
+    w = make_workload("c2", num_reqs=2, ctx_args=(900, 1500), budget=16 * 8, ar_queries=True)
+    c = w.cfg
+    hk_t, hv_t = pinned_pages(w)
+    d = _dims(w)
+    k = c.K
+    ctx_d = dev_i32(w.ctx_len(0))
+    qs = [dev_bf16(x) for x in w.layer_queries(0, 3)]
+    path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=3, streams=pair)
+    st = LayerState(d, c.T, k)
+    path.build_summaries(st, ctx_d)
+    path.predict(st, qs[0], ctx_d)
+    path.stage(st, ctx_d, 0, fetch_cap=k)
+    note("wait fault: normal pipelined step")
+    path.step_pipelined(st, qs[1], ctx_d, 1)
+    path.join()
+    path.check()
+    P.oasis_pipeline_set_wait_limit(path._pipe, 64)
+    note("wait fault: stalled prediction stream, wait bound 64 polls")
+    with torch.cuda.stream(path.side):
+        torch.cuda._sleep(200_000_000)  # a bounded spin ahead of the prediction's kernels
+    path.step_pipelined(st, qs[2], ctx_d, 2)
+    path.join()
+    with pytest.raises(P.OasisError, match="gave up waiting"):
+        path.check()
+    with pytest.raises(P.OasisError, match="gave up waiting"):
+        path.close()  # reports it again and still releases the issuer
+    assert path._pipe is None
 
 
 @pytest.mark.parametrize("plan_pred", [False, True])

@@ -96,6 +96,9 @@ def parse():
     ap.add_argument("--fused-prediction", choices=("auto", "off", "on"), default="auto",
                     help="score and select (and plan) in one kernel per step: auto = with >= 256 (request, KV head) "
                          "pairs")
+    ap.add_argument("--prediction-order", choices=("auto", "beside", "after"), default="auto",
+                    help="start each step's prediction beside its attention or after it (auto: after for at most "
+                         "64 (request, KV head) pairs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention comparison")
@@ -117,6 +120,12 @@ def plan_on_prediction(args) -> bool:
     if args.plan_stream == "auto":
         return args.workload == "c3"
     return args.plan_stream == "prediction"
+
+
+def prediction_order(args) -> int:
+    from paper_2608_08097_amd import _lib as L
+    return {"auto": L.PREDICT_AUTO, "beside": L.PREDICT_BESIDE_ATTENTION,
+            "after": L.PREDICT_AFTER_ATTENTION}[args.prediction_order]
 
 
 def fused_mode(args) -> int:
@@ -288,10 +297,10 @@ def cpu_baseline(w, hk, hv, queries, k, fetch_cap, budget_s):
         state = list(ex.map(fill, range(c.num_reqs)))   # setup, not timed
         step = 0
 
-        def sample(seconds, pool):
+        def sample(seconds, pool, last):
             nonlocal step
             steps, spent = 0, 0.0
-            while spent < seconds and step + 1 < len(queries):
+            while spent < seconds and step < last:
                 step += 1
                 t0 = time.perf_counter()
                 if pool is None:
@@ -303,8 +312,10 @@ def cpu_baseline(w, hk, hv, queries, k, fetch_cap, budget_s):
                 steps += 1
             return steps, spent
 
-        n1, t1 = sample(budget_s / 3, None)
-        nw, tw = sample(2 * budget_s / 3, ex)
+        # steps 1 .. len(queries) - 1: at most half of them on one thread, the rest on the workers
+        n_steps = len(queries) - 1
+        n1, t1 = sample(budget_s / 3, None, n_steps // 2)
+        nw, tw = sample(2 * budget_s / 3, ex, n_steps)
     return {"value": nw / tw, "unit": "steps/s", "cores": workers, "kind": "oracle",
             "host_cores": cores, "blas_threads_per_worker": 1, "blas_threads_default": blas_default,
             "value_1_thread": n1 / t1,
@@ -364,7 +375,7 @@ def main():
     fetch_cap = K if args.fetch_ratio >= 1.0 else max(1, int(math.floor(args.fetch_ratio * K)))
     path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=fetch_cap,
                       plan_on_prediction=plan_on_prediction(args),
-                      fused_prediction=fused_mode(args))
+                      fused_prediction=fused_mode(args), prediction_order=prediction_order(args))
     layers = [path.new_layer() for _ in range(NL)]
     path.build_summaries(layers[0], ctx_d)
     for st in layers[1:]:
@@ -470,6 +481,7 @@ def main():
             "fetch_ratio": args.fetch_ratio if fetch_cap < K else "all", "fetch_cap": fetch_cap,
             "parallelism": "single GPU", "plan_stream": "prediction" if plan_on_prediction(args) else "transfer",
             "fused_prediction": args.fused_prediction,
+            "prediction_order": args.prediction_order,
             "gpu_max_hw_queues": HW_QUEUES if HW_QUEUES is not None else "unset (HIP default, 4)",
         },
         "roofline": {
@@ -541,7 +553,7 @@ def run_reasoning(args, P, torch, DecodePath):
     ctx_d = [torch.from_numpy(w.ctx_len(s_)).cuda() for s_ in range(S)]
     path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=fetch_cap,
                       max_layers=NL, plan_on_prediction=plan_on_prediction(args),
-                      fused_prediction=fused_mode(args))
+                      fused_prediction=fused_mode(args), prediction_order=prediction_order(args))
     # The blocks that are a request's local block during the run live in device
     # pages, as a model writes its newest tokens on the GPU: the local refresh
     # and the compressed-key update of a completed block read them there, and
@@ -617,6 +629,7 @@ def run_reasoning(args, P, torch, DecodePath):
                    "global_batch": c.num_reqs, "layers": NL, "fetch_cap": fetch_cap,
                    "plan_stream": "prediction" if plan_on_prediction(args) else "transfer",
                    "fused_prediction": args.fused_prediction,
+                   "prediction_order": args.prediction_order,
                    "gpu_max_hw_queues": HW_QUEUES if HW_QUEUES is not None else "unset (HIP default, 4)"},
         "tokens_per_s": round(c.num_reqs * S / elapsed, 1),
         "decode_step_ms_all_layers": round(t_step_us / 1e3, 3),
@@ -646,7 +659,7 @@ def budget_sweep(P, torch, DecodePath, d, c, w, hk_t, hv_t, bt, layers, qs, ctx_
         K = budget // c.block_size
         cap = K if args.fetch_ratio >= 1.0 else max(1, int(math.floor(args.fetch_ratio * K)))
         path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=cap,
-                          streams=streams)
+                          streams=streams, prediction_order=prediction_order(args))
         sts = []
         for l in range(NL):
             st = LayerState(d, c.T, K)
@@ -690,7 +703,7 @@ def fetch_sweep(P, torch, DecodePath, d, c, K, hk_t, hv_t, bt, layers, qs, ctx_d
     for ratio in (0.01, 0.02, 0.05, 0.10, 0.20, 1.0):
         cap = K if ratio >= 1.0 else max(1, int(math.floor(ratio * K)))
         path = DecodePath(d, c.T, K, hk_t.view(torch.bfloat16), hv_t.view(torch.bfloat16), bt, fetch_cap=cap,
-                          streams=streams)
+                          streams=streams, prediction_order=prediction_order(args))
         for l, st in enumerate(layers):
             st.reset()
             path.predict(st, qs[l][0], ctx_d)

@@ -445,6 +445,23 @@ OASIS_API oasis_status oasis_pipeline_set_plan_stream(oasis_pipeline* pipeline, 
 #define OASIS_FUSED_PREDICTION_ON 2
 OASIS_API oasis_status oasis_pipeline_set_fused_prediction(oasis_pipeline* pipeline, int32_t mode);
 
+/* Where a step's prediction (scoring and top-K on the prediction stream)
+ * starts. OASIS_PREDICT_BESIDE_ATTENTION (paper §4.2.2: the prediction runs
+ * in the background beside the foreground's attention): once the step's
+ * queries are ready, and the transfer waits for the prediction and for the
+ * attention. OASIS_PREDICT_AFTER_ATTENTION: once the step's attention has
+ * finished, and the transfer waits for the prediction alone; one
+ * cross-stream edge fewer, and the bandwidth-bound scorer no longer shares
+ * HBM with this attention (it still runs beside the next layers'). The
+ * results are the same either way; which is faster depends on the shapes.
+ * OASIS_PREDICT_AUTO (default): after the attention for at most 64
+ * (request, KV head) pairs, beside it otherwise. Takes effect from the next
+ * step. Errors: INVALID_ARG for a NULL pipeline or another value. */
+#define OASIS_PREDICT_AUTO 0
+#define OASIS_PREDICT_BESIDE_ATTENTION 1
+#define OASIS_PREDICT_AFTER_ATTENTION 2
+OASIS_API oasis_status oasis_pipeline_set_prediction_order(oasis_pipeline* pipeline, int32_t order);
+
 /* Issue one decode step of `layer` (see above). q: bf16 device [R][T][Hq][d];
  * ctx_len: device [R]; prev_ctx_len (nullable, device [R]): the lengths at the
  * layer's previous step; when set, the compressed keys of the blocks completed

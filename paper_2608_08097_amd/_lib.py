@@ -29,6 +29,7 @@ EXPORTS = (
     "oasis_pipeline_create", "oasis_pipeline_set_layer", "oasis_pipeline_set_local_source",
     "oasis_pipeline_set_plan_stream", "oasis_pipeline_set_fused_prediction", "oasis_pipeline_step",
     "oasis_pipeline_join", "oasis_pipeline_check", "oasis_pipeline_set_wait_limit",
+    "oasis_pipeline_set_prediction_order",
     "oasis_pipeline_destroy", "oasis_pipeline_profile_begin", "oasis_pipeline_profile_end",
 )
 
@@ -126,6 +127,8 @@ def lib() -> ctypes.CDLL:
         L.oasis_pipeline_join.argtypes = [_P, _P]
         L.oasis_pipeline_check.restype = _I32
         L.oasis_pipeline_check.argtypes = [_P]
+        L.oasis_pipeline_set_prediction_order.restype = _I32
+        L.oasis_pipeline_set_prediction_order.argtypes = [_P, _I32]
         L.oasis_pipeline_set_wait_limit.restype = _I32
         L.oasis_pipeline_set_wait_limit.argtypes = [_P, ctypes.c_uint32]
         L.oasis_pipeline_destroy.restype = None
@@ -477,6 +480,16 @@ def oasis_pipeline_join(handle: int, stream=None) -> None:
 def oasis_pipeline_check(handle: int) -> None:
     """Synchronize the device; raise if a transfer of the pipeline gave up waiting for its prediction."""
     _check("oasis_pipeline_check", lib().oasis_pipeline_check(handle))
+
+
+PREDICT_AUTO = 0              # OASIS_PREDICT_AUTO
+PREDICT_BESIDE_ATTENTION = 1  # OASIS_PREDICT_BESIDE_ATTENTION
+PREDICT_AFTER_ATTENTION = 2   # OASIS_PREDICT_AFTER_ATTENTION
+
+
+def oasis_pipeline_set_prediction_order(handle: int, order: int) -> None:
+    """Start each step's prediction beside or after its attention (PREDICT_AUTO: by the pair count)."""
+    _check("oasis_pipeline_set_prediction_order", lib().oasis_pipeline_set_prediction_order(handle, int(order)))
 
 
 def oasis_pipeline_set_wait_limit(handle: int, polls: int) -> None:

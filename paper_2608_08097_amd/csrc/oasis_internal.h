@@ -169,12 +169,12 @@ struct StageArgs {
   // copy the entries in `ws` and commit its rows to slot_map / slot_stamp.
   int mode;
   int32_t* ws;              // stage_ws_ints(R * Hkv, k) ints (modes 1 and 2)
-  // When wait_flag is set, the staging kernel first waits until *wait_flag >=
-  // wait_value (a counter that another stream's work raises): one thread of
-  // each workgroup polls it, at most wait_polls times; past that the
-  // workgroup stores 1 to *wait_fault and goes on.
-  const uint32_t* wait_flag;
-  uint32_t wait_value;
+  // For each wait_flag[i] that is set, the staging kernel first waits until
+  // *wait_flag[i] >= wait_value[i] (counters that other streams' work raises):
+  // one thread of each workgroup polls them, at most wait_polls times in all;
+  // past that the workgroup stores 1 to *wait_fault and goes on.
+  const uint32_t* wait_flag[2];
+  uint32_t wait_value[2];
   uint32_t* wait_fault;
   uint32_t wait_polls;
 };

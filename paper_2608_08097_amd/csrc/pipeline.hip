@@ -21,12 +21,18 @@
 
 namespace {
 constexpr int kFlagStride = 64;  // uint32 per counter (256 bytes)
-constexpr int kQ = 0, kPred = 1, kJoinPred = 2, kJoinXfer = 3, kStaged0 = 4;  // counter slots
+constexpr int kQ = 0, kPred = 1, kAttn = 2, kJoinPred = 3, kJoinXfer = 4, kStaged0 = 5;  // counter slots
 constexpr uint32_t kWrapGuard = 1u << 30;
 constexpr int kProfKinds = 4;  // attention (split + merge), scoring, top-K, staging
 // (request, KV head) pairs from which OASIS_FUSED_PREDICTION_AUTO scores and
 // selects in one kernel (one 1024-thread workgroup per pair: a full chip)
 constexpr long long kFusedMinPairs = 256;
+// (request, KV head) pairs up to which OASIS_PREDICT_AUTO starts the prediction
+// after the attention (measured on MI355X, steps/s beside / after: 1 pair x
+// 8,192 tokens 30,311 / 32,119; 64 pairs x 131,072 tokens 10,922 / 11,212;
+// 128 pairs x 65,536 tokens 3,971 / 3,188; 256 pairs 9,543 / 9,116; the
+// 32-layer loop of 512 pairs 3,543 / 3,466 layer-steps/s)
+constexpr long long kAfterMaxPairs = 64;
 }  // namespace
 
 struct oasis_pipeline {
@@ -54,6 +60,7 @@ struct oasis_pipeline {
   bool plan_on_pred;            // OASIS_PLAN_ON_PREDICTION
   int32_t fused_pred;           // OASIS_FUSED_PREDICTION_*: score and top-K (+ plan) in one kernel
   uint32_t wait_polls;          // bound of the staging kernel's wait for its prediction
+  int32_t pred_order;           // OASIS_PREDICT_*: where a step's prediction starts
   // optional profile: timing events around each kernel of the next prof_cap steps
   int32_t prof_cap, prof_n;
   hipEvent_t* prof_ev;          // [prof_cap][kProfKinds][2]
@@ -223,6 +230,7 @@ oasis_status oasis_pipeline_create(const oasis_dims* dims, int32_t num_q_tokens,
   p->local_block_table = host_block_table;
   p->max_layers = max_layers;
   p->wait_polls = oasis::kStageWaitSpins;
+  p->pred_order = OASIS_PREDICT_AUTO;
   p->layers = new (std::nothrow) oasis_layer_buffers[max_layers]();
   p->staged = new (std::nothrow) uint32_t[max_layers]();
   p->is_set = new (std::nothrow) bool[max_layers]();
@@ -326,6 +334,15 @@ oasis_status oasis_pipeline_set_wait_limit(oasis_pipeline* p, uint32_t polls) {
   return ok();
 }
 
+oasis_status oasis_pipeline_set_prediction_order(oasis_pipeline* p, int32_t order) {
+  static const char* fn = "oasis_pipeline_set_prediction_order";
+  if (!p) return fail(OASIS_ERR_INVALID_ARG, "%s: pipeline is NULL", fn);
+  if (order != OASIS_PREDICT_AUTO && order != OASIS_PREDICT_BESIDE_ATTENTION && order != OASIS_PREDICT_AFTER_ATTENTION)
+    return fail(OASIS_ERR_INVALID_ARG, "%s: order = %d is not an OASIS_PREDICT_* value", fn, order);
+  p->pred_order = order;
+  return ok();
+}
+
 oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_t* q, const int32_t* ctx_len,
                                  const int32_t* prev_ctx_len, int32_t max_new_blocks, int32_t step, int32_t growing,
                                  int32_t* moved, void* stream) {
@@ -386,15 +403,27 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
   const int sl = kStaged0 + layer;
   // foreground: this layer's previous transfer must have landed before its attention
   if (p->staged[layer]) HIP_TRY(wait_for(p, fg, sl, p->staged[layer]), fn);
+  // kQ: q and ctx_len are ready on the foreground; past the wait above this
+  // also means the previous transfer has finished reading sel and scores (which
+  // the prediction rewrites). kAttn: the attention is done with the pool slots
+  // this step's gather overwrites. Beside the attention, the prediction starts
+  // at kQ and the transfer waits for both counters; after it, one counter
+  // raised after the attention serves as both (the transfer waits for the
+  // prediction, which waited for the attention).
+  const bool beside = p->pred_order == OASIS_PREDICT_BESIDE_ATTENTION ||
+                      (p->pred_order == OASIS_PREDICT_AUTO && (long long)d->num_reqs * d->num_kv_heads > kAfterMaxPairs);
+  if (beside) {
+    HIP_TRY(signal_next(p, fg, kQ, &cnt[kQ]), fn);
+    HIP_TRY(wait_for(p, p->pred, kQ, cnt[kQ]), fn);
+  }
   if (growing) HIP_TRY(oasis::launch_stage(la, fg), fn);
   HIP_TRY(oasis::launch_attn(aa, fg, prof_timing(p, 0)), fn);
-  // One edge from the foreground, after the attention: q and ctx_len are
-  // ready; past the wait above, the previous transfer has finished reading sel
-  // and scores (which the prediction rewrites); and the attention is done with
-  // the pool slots this step's gather overwrites (the transfer is ordered
-  // behind the prediction, which is ordered behind this).
-  HIP_TRY(signal_next(p, fg, kQ, &cnt[kQ]), fn);
-  HIP_TRY(wait_for(p, p->pred, kQ, cnt[kQ]), fn);
+  if (beside) {
+    HIP_TRY(signal_next(p, fg, kAttn, &cnt[kAttn]), fn);
+  } else {
+    HIP_TRY(signal_next(p, fg, kQ, &cnt[kQ]), fn);
+    HIP_TRY(wait_for(p, p->pred, kQ, cnt[kQ]), fn);
+  }
   if (prev_ctx_len) HIP_TRY(oasis::launch_summaries(ua, p->pred), fn);
   // one workgroup per (request, KV head) scores and selects (and plans) when
   // the rows are many and short enough to fill the chip that way
@@ -416,10 +445,12 @@ oasis_status oasis_pipeline_step(oasis_pipeline* p, int32_t layer, const uint16_
       HIP_TRY(oasis::launch_topk(ta, p->pred, prof_timing(p, 2)), fn);
   }
   HIP_TRY(signal_next(p, p->pred, kPred, &cnt[kPred]), fn);
-  // the transfer waits for the prediction inside its own kernel (no stream-wait
-  // dispatch on the stream that paces the step)
-  ga.wait_flag = slot(p, kPred);
-  ga.wait_value = cnt[kPred];
+  // the transfer waits for the prediction and for the attention inside its own
+  // kernel (no stream-wait dispatch on the stream that paces the step)
+  ga.wait_flag[0] = slot(p, kPred);
+  ga.wait_value[0] = cnt[kPred];
+  ga.wait_flag[1] = beside ? slot(p, kAttn) : nullptr;
+  ga.wait_value[1] = beside ? cnt[kAttn] : 0;
   ga.wait_fault = fault_word(p);
   ga.wait_polls = p->wait_polls;
   HIP_TRY(oasis::launch_stage(ga, p->xfer, prof_timing(p, 3)), fn);

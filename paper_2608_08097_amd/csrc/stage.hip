@@ -536,23 +536,26 @@ __device__ __forceinline__ void copy_entries(const StageArgs& a, int n, const in
   }
 }
 
-// The in-kernel form of a stream wait on a counter (StageArgs::wait_flag): it
-// saves the transfer stream a dispatch per step. Thread 0 polls with relaxed
+// The in-kernel form of stream waits on counters (StageArgs::wait_flag): it
+// saves the transfer stream a dispatch per counter and step. Thread 0 polls with relaxed
 // agent-scope loads; the barrier holds the other waves; the acquire fence then
 // orders every later read after the producer's writes, which its kernel's end
 // released before the counter was raised. The poll is bounded (wait_polls, a
 // few seconds by default): a counter that is never raised costs that time and
 // a fault mark, not a hang.
 __device__ __forceinline__ void stage_wait(const StageArgs& a) {
-  if (!a.wait_flag) return;
+  if (!a.wait_flag[0] && !a.wait_flag[1]) return;
   if (threadIdx.x == 0) {
     uint32_t n = 0;
-    while (__hip_atomic_load(a.wait_flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < a.wait_value) {
-      if (++n >= a.wait_polls) {
-        __hip_atomic_store(a.wait_fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        break;
+    for (int i = 0; i < 2; ++i) {
+      if (!a.wait_flag[i]) continue;
+      while (__hip_atomic_load(a.wait_flag[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < a.wait_value[i]) {
+        if (++n >= a.wait_polls) {
+          __hip_atomic_store(a.wait_fault, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
       }
-      __builtin_amdgcn_s_sleep(2);
     }
   }
   __syncthreads();

@@ -129,7 +129,7 @@ class DecodePath:
                  block_table: torch.Tensor, first_draft: int = 1, num_draft: int | None = None,
                  scale: float | None = None, fetch_cap: int | None = None, native: bool = True,
                  max_layers: int = 256, streams: tuple | None = None, plan_on_prediction: bool = False,
-                 fused_prediction: int | None = None):
+                 fused_prediction: int | None = None, prediction_order: int | None = None):
         self.dims, self.T, self.k = d, int(num_q_tokens), int(k)
         # native issuer: plan each step's transfer in the top-K kernel on the
         # prediction stream instead of in the staging kernel on the transfer stream
@@ -137,6 +137,8 @@ class DecodePath:
         # native issuer: score and select (and plan) in one kernel per step (L.FUSED_PREDICTION_*;
         # None keeps the library's default, AUTO)
         self.fused_prediction = fused_prediction
+        # native issuer: where each step's prediction starts (L.PREDICT_*; None keeps AUTO)
+        self.prediction_order = prediction_order
         # step_pipelined issues through the library's native step issuer unless a timer is given
         self.native = bool(native)
         self.max_layers = int(max_layers)
@@ -170,6 +172,8 @@ class DecodePath:
                 L.oasis_pipeline_set_plan_stream(self._pipe, L.PLAN_ON_PREDICTION)
             if self.fused_prediction is not None:
                 L.oasis_pipeline_set_fused_prediction(self._pipe, self.fused_prediction)
+            if self.prediction_order is not None:
+                L.oasis_pipeline_set_prediction_order(self._pipe, self.prediction_order)
         lid = getattr(st, "layer_id", None)
         if lid is None or getattr(st, "pipe", None) != self._pipe:
             if self._n_layers >= self.max_layers:

@@ -141,6 +141,7 @@ def test_score_select_checks_without_gpu(lib):
     assert L.oasis_score_select(ctypes.byref(ok), None, 5, 1, 4, P[1], P[2], P[3], 64, P[4], P[5], P[0], None) == 1
     assert L.oasis_pipeline_set_fused_prediction(None, 0) == 1
     assert L.oasis_pipeline_set_wait_limit(None, 5) == 1
+    assert L.oasis_pipeline_set_prediction_order(None, 0) == 1
     assert L.oasis_pipeline_check(None) == 1
 
 

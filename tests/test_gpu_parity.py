@@ -568,14 +568,15 @@ def test_pipelined_multistep(cap, issue):
             assert moved.max() <= cap
 
 
+@pytest.mark.parametrize("order", ["beside", "after"])
 @pytest.mark.parametrize("plan_pred", [False, True])
 @pytest.mark.parametrize("fused", [False, True])
-def test_pipelined_layers_native(plan_pred, fused):
+def test_pipelined_layers_native(plan_pred, fused, order):
     """Several layers interleaved on the native issuer with no host synchronization
     between steps (paper §4.2.2: per-layer chains, layer-local waits); every
     layer's final state equals its own oracle chain, with the transfer planned on
-    either stream, and the prediction by the separate kernels or by the fused
-    score + select (+ plan) kernel."""
+    either stream, the prediction by the separate kernels or by the fused
+    score + select (+ plan) kernel, and started beside or after the attention."""
     n_layers, rounds, cap = 3, 4, 3
     w = make_workload("c2", num_reqs=3, ctx_args=(900, 2500), budget=16 * 20, ar_queries=True)
     c = w.cfg
@@ -588,7 +589,8 @@ def test_pipelined_layers_native(plan_pred, fused):
     qs = [w.layer_queries(l, rounds + 1) for l in range(n_layers)]
     kmax, kmin = O.block_summaries(hk, w.block_table, ctx, c.block_size, w.NBmax)
     path = DecodePath(d, c.T, k, hk_t, hv_t, dev_i32(w.block_table), fetch_cap=cap, plan_on_prediction=plan_pred,
-                      fused_prediction=P.FUSED_PREDICTION_ON if fused else P.FUSED_PREDICTION_OFF)
+                      fused_prediction=P.FUSED_PREDICTION_ON if fused else P.FUSED_PREDICTION_OFF,
+                      prediction_order=P.PREDICT_BESIDE_ATTENTION if order == "beside" else P.PREDICT_AFTER_ATTENTION)
     layers = [LayerState(d, c.T, k) for _ in range(n_layers)]
     ref = []
     for l, st in enumerate(layers):
@@ -605,7 +607,8 @@ def test_pipelined_layers_native(plan_pred, fused):
         O.stage_blocks(hk, hv, w.block_table, sel, cnt, smap, stamp, 0, pk, pv, ctx, c.block_size)
         ref.append(dict(smap=smap, stamp=stamp, pk=pk, pv=pv))
     q_dev = [[dev_bf16(x) for x in qs[l]] for l in range(n_layers)]
-    note(f"native pipelined layers: issuing (plan on prediction: {plan_pred}, fused prediction: {fused})")
+    note(f"native pipelined layers: issuing (plan on prediction: {plan_pred}, fused prediction: {fused}, "
+         f"prediction {order} the attention)")
     for s in range(1, rounds + 1):
         for l in range(n_layers):
             path.step_pipelined(layers[l], q_dev[l][s], ctx_d, s)

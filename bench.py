@@ -316,9 +316,12 @@ def cpu_baseline(w, hk, hv, queries, k, fetch_cap, budget_s):
         n_steps = len(queries) - 1
         n1, t1 = sample(budget_s / 3, None, n_steps // 2)
         nw, tw = sample(2 * budget_s / 3, ex, n_steps)
-    return {"value": nw / tw, "unit": "steps/s", "cores": workers, "kind": "oracle",
+    # the faster of the two arrangements is the baseline (for many small requests the worker
+    # threads mostly contend for the interpreter)
+    r_w, r_1 = nw / tw, n1 / t1
+    return {"value": max(r_w, r_1), "unit": "steps/s", "cores": workers if r_w >= r_1 else 1, "kind": "oracle",
             "host_cores": cores, "blas_threads_per_worker": 1, "blas_threads_default": blas_default,
-            "value_1_thread": n1 / t1,
+            "value_workers": r_w, "value_1_thread": r_1,
             "sample": f"whole decode steps of all {c.num_reqs} requests (scores, top-K, delta staging with fetch "
                       f"cap {fetch_cap}, attention; after an untimed initial fill) in float64 NumPy: {nw} steps in "
                       f"{tw:.1f} s with the requests on {workers} worker threads (host has {cores} cores), then "

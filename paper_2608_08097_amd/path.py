@@ -44,7 +44,7 @@ class LayerState:
         self.ev_staged = None   # recorded after the last stage of this layer
         self.ev_attended = None  # recorded after the last attention of this layer
         self.layer_id = None    # id in the native issuer of the DecodePath that runs it
-        self.pipe = None
+        self.pipe_token = None  # the native issuer this layer is registered with
 
     def reset(self):
         self.slot_map.fill_(-1)
@@ -143,6 +143,7 @@ class DecodePath:
         self.native = bool(native)
         self.max_layers = int(max_layers)
         self._pipe = None
+        self._pipe_token = None
         self._n_layers = 0
         # admitted misses per (request, KV head) and step; k admits every miss
         self.fetch_cap = self.k if fetch_cap is None else int(fetch_cap)
@@ -174,8 +175,10 @@ class DecodePath:
                 L.oasis_pipeline_set_fused_prediction(self._pipe, self.fused_prediction)
             if self.prediction_order is not None:
                 L.oasis_pipeline_set_prediction_order(self._pipe, self.prediction_order)
+            # identifies this issuer: a later one may be created at the same address
+            self._pipe_token = object()
         lid = getattr(st, "layer_id", None)
-        if lid is None or getattr(st, "pipe", None) != self._pipe:
+        if lid is None or getattr(st, "pipe_token", None) is not self._pipe_token:
             if self._n_layers >= self.max_layers:
                 raise RuntimeError(f"more than {self.max_layers} layers on one DecodePath")
             lid = self._n_layers
@@ -183,7 +186,7 @@ class DecodePath:
             L.oasis_pipeline_set_layer(self._pipe, lid, self.dims, self.T, self.k, st.kmax, st.kmin, st.scores,
                                        st.sel, st.sel_count, st.slot_map, st.slot_stamp, st.pool_k, st.pool_v,
                                        st.moved, st.out, st.lse, st.ws_attn)
-            st.layer_id, st.pipe = lid, self._pipe
+            st.layer_id, st.pipe_token = lid, self._pipe_token
         return lid
 
     def set_plan_on_prediction(self, on: bool):

@@ -420,6 +420,9 @@ ATTN_CASES = [
     (13, 2, 64, 8, 9, 16, 70, [3000, 1111], 0.3),        # 72 rows, five row tiles, B = 16
     # 256 (request, KV head) pairs: one split each, the many-row kernel writes the outputs itself
     (14, 32, 64, 8, 9, 32, 6, [6 * 32 + 5 + 3 * r for r in range(32)], 0.2),
+    (15, 2, 64, 8, 9, 16, 0, [10, 1], 0.0),               # many-row kernel, local block only
+    (16, 2, 64, 8, 9, 32, 16, [0, 300], 1.0),             # many-row kernel, empty context; all slots free
+    (17, 3, 40, 8, 8, 16, 7, [100, 17, 16], 0.3),         # many-row kernel, odd unit tail, local_len 1 and 16
 ]
 
 

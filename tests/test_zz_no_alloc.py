@@ -1,6 +1,6 @@
 """The allocation-free attention entry point (library scratch instead of a workspace) against the
 workspace entry point, through the C ABI: two calls in a row, the second with smaller sizes, then the
-first again. Same kernels, so the outputs must be bit-identical; they are also checked against the
+first again (and a many-row shape before them). Same kernels, so the outputs must be bit-identical; they are also checked against the
 oracle at the attention tolerance."""
 import numpy as np
 import pytest
@@ -42,9 +42,11 @@ def _both(q, pk, pv, smap, ctx, R, Hq, Hkv, T, B, ks):
 
 
 def test_noalloc_matches_workspace_entry_point():
+    rows72 = dict(R=4, Hq=64, Hkv=8, T=9, B=32, ks=32)               # 32 pairs x 8 splits x 72 rows (many-row kernel)
     big = dict(R=8, Hq=32, Hkv=8, T=5, B=16, ks=128)                 # 64 pairs x 4 splits x 20 rows
     small = dict(R=2, Hq=16, Hkv=8, T=3, B=32, ks=32)                # 16 pairs x 9 splits x 6 rows
-    cases = [(1, big, [2064, 1800, 2050, 33, 2064, 1999, 2048, 2063]), (2, small, [1040, 600])]
+    cases = [(3, rows72, [1056, 900, 33, 1040]), (1, big, [2064, 1800, 2050, 33, 2064, 1999, 2048, 2063]),
+             (2, small, [1040, 600])]
     first = None
     for seed, sz, lens in cases + [cases[0]]:
         q, pk, pv, smap, ctx = _inputs(seed, lens=lens, **sz)

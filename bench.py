@@ -99,6 +99,9 @@ def parse():
     ap.add_argument("--prediction-order", choices=("auto", "beside", "after"), default="auto",
                     help="start each step's prediction beside its attention or after it (auto: after for at most "
                          "64 (request, KV head) pairs)")
+    ap.add_argument("--tp-share", type=int, default=1,
+                    help="one GPU's share of an N-way tensor-parallel deployment: KV and query heads divided by N "
+                         "(a shape probe of the same kernels; design only beyond one GPU)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the oracle sample")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense-attention comparison")
@@ -358,7 +361,13 @@ def main():
     total_steps = args.warmup + args.steps
     NL = max(1, args.layers)
     per_layer_steps = (total_steps + args.steps + NL - 1) // NL  # queries of both timed regions
-    cfg = config(args.workload, budget=args.budget, ar_queries=True, steps=per_layer_steps, grow_per_step=0)
+    base = config(args.workload)
+    if args.tp_share < 1 or base.num_kv_heads % args.tp_share:
+        raise SystemExit(f"--tp-share {args.tp_share} must divide the {base.num_kv_heads} KV heads")
+    heads = {} if args.tp_share == 1 else dict(num_kv_heads=base.num_kv_heads // args.tp_share,
+                                               num_q_heads=base.num_q_heads // args.tp_share)
+    cfg = config(args.workload, budget=args.budget, ar_queries=True, steps=per_layer_steps, grow_per_step=0,
+                 **heads)
     w = Workload(cfg)
     c = w.cfg
     K = c.K
@@ -486,6 +495,7 @@ def main():
             "fused_prediction": args.fused_prediction,
             "prediction_order": args.prediction_order,
             "gpu_max_hw_queues": HW_QUEUES if HW_QUEUES is not None else "unset (HIP default, 4)",
+            "tp_share": args.tp_share,
         },
         "roofline": {
             "bound": "hbm", "kernel": "score_kernel (oasis_score_blocks)",

@@ -229,8 +229,11 @@ __device__ __forceinline__ int unit_slot(int u_first, int t0, int lane) {
   const int j = BS == 16 ? lane >> 1 : lane;
   return BS == 16 ? 2 * (u_first + (t0 + j) * kW) + (lane & 1) : u_first + (t0 + j) * kW;
 }
+__device__ __forceinline__ const int32_t* map_addr(const int32_t* smap, int ks, int slot, const int32_t* fallback) {
+  return ks > 0 ? smap + (slot < ks ? slot : ks - 1) : fallback;
+}
 __device__ __forceinline__ int map_load(const int32_t* smap, int ks, int slot, const int32_t* fallback) {
-  return *(ks > 0 ? smap + (slot < ks ? slot : ks - 1) : fallback);
+  return *map_addr(smap, ks, slot, fallback);
 }
 __device__ __forceinline__ uint64_t map_mask(int ks, int slot, int entry) {
   return __builtin_amdgcn_ballot_w64(slot < ks && entry >= 0);
@@ -442,12 +445,14 @@ __global__ __launch_bounds__(kW * 64) void attn_split_kernel(AttnArgs a) {
 // Measured on MI355X (16 requests x 8 KV heads x 72 rows, B = 32, 4,096
 // tokens per head, 268 MB): 81.7 us for the register kernel (every wave loads
 // the units of its own split range, five row tiles per wave), 63 to 66 us here
-// with the merge; 1 to 2 us less again with each unit's score products issued
-// one step ahead of its softmax and PV products (below). Registers staged through VGPRs instead of direct-to-LDS
-// loads, two units ahead: 67 to 70 us; six stages instead of four, or two
-// workgroups per CU: no gain. The loads alone (no arithmetic) take 57 to 60
-// us against 48 us for a plain streaming read of the same bytes.
-constexpr int kRowsStages = 4;
+// with the merge and four stages; 1 to 2 us less with each unit's score
+// products issued one step ahead of its softmax and PV products (below),
+// about 1 us less again with the prologue's own loads on the DMA path
+// (below), and 0.5 to 1.5 us less again with three stages instead of four
+// (two: 80 us; six: no gain). Registers staged through VGPRs instead of
+// direct-to-LDS loads, two units ahead: 67 to 70 us; two workgroups per CU: no
+// gain; exact per-wave load counts instead of the surplus loads: 1 us slower.
+constexpr int kRowsStages = 3;
 typedef u32x4 UnitLds[17][64];  // [chunk][lane]; chunk 16 takes the surplus loads
 
 template <int BS>
@@ -492,6 +497,22 @@ __device__ __forceinline__ void lds_dma16(const void* gsrc, void* lds_row) {
       "s_mov_b32 m0, %2\n\t"
       "s_nop 0\n\t"
       "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(gsrc), "s"(lds)
+      : "memory");
+}
+
+// 4 bytes a lane, as lds_dma16 (lane L's bytes land at lds_row + 4 L).
+__device__ __forceinline__ void lds_dma4(const void* gsrc, void* lds_row) {
+  const uint32_t lds =
+      __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)lds_row);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dword %1, off\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
       : "v"(gsrc), "s"(lds)
@@ -579,7 +600,7 @@ __device__ __forceinline__ void unit_softmax_pv(const f32x4 (&sc)[2], const u32x
 
 template <int NT, int BS>
 __global__ __launch_bounds__(NT * 64) void attn_split_rows_kernel(AttnArgs a) {
-  static_assert(kRowsStages == 4, "one LDS variable per stage below");
+  static_assert(kRowsStages == 3, "one LDS variable per stage below");
   constexpr int kPer = (16 + NT - 1) / NT;  // chunk loads per wave and unit
   // One LDS variable per stage, always named with a compile-time stage, so the
   // compiler sees each read of a stage apart from the other stages' loads.
@@ -588,13 +609,13 @@ __global__ __launch_bounds__(NT * 64) void attn_split_rows_kernel(AttnArgs a) {
   __shared__ __align__(16) UnitLds s_st0;
   __shared__ __align__(16) UnitLds s_st1;
   __shared__ __align__(16) UnitLds s_st2;
-  __shared__ __align__(16) UnitLds s_st3;
+  __shared__ __align__(16) u32x4 s_q[NT][4][64];  // each wave's query operand (4 k-steps)
+  __shared__ int s_misc[NT][3][64];               // each wave's context length and two mask chunks
   auto stage_buf = [&](auto S) __attribute__((always_inline)) -> UnitLds& {
     constexpr int k = decltype(S)::value;
     if constexpr (k == 0) return s_st0;
     else if constexpr (k == 1) return s_st1;
-    else if constexpr (k == 2) return s_st2;
-    else return s_st3;
+    else return s_st2;
   };
   const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // this wave's row tile
   const int lane = threadIdx.x & 63;
@@ -633,31 +654,38 @@ __global__ __launch_bounds__(NT * 64) void attn_split_rows_kernel(AttnArgs a) {
     const int jj = BS == 16 ? lane >> 1 : lane;
     return BS == 16 ? 2 * (u_begin + t + jj) + (lane & 1) : u_begin + t + jj;
   };
-  const int slot0 = mask_slot(0);
-  const int entry0 = map_load(smap, ks, slot0, a.ctx_len + r);
+  // Everything else the unit loop reads (the context length, the slot-map
+  // entries of the first two mask chunks, this wave's query operand) takes the
+  // same LDS-DMA path, ahead of the ring's first units: the compiler cannot
+  // count the DMA loads, so its wait for any load it issues after them would
+  // drain the ring. Rows past the end load row 0's queries and are zeroed.
+  const int row = v * 16 + i;
+  {
+    const int qr = row < a.rows ? row : 0;
+    const int tq = qr / a.G;
+    const int qh = h * a.G + (qr - tq * a.G);
+    const uint16_t* qrow = a.q + (((long long)r * a.T + tq) * a.Hq + qh) * kHeadDim;
+    lds_dma4(a.ctx_len + r, &s_misc[v][0][0]);
+    lds_dma4(map_addr(smap, ks, mask_slot(0), a.ctx_len + r), &s_misc[v][1][0]);
+    lds_dma4(map_addr(smap, ks, mask_slot(kChunkU), a.ctx_len + r), &s_misc[v][2][0]);
+#pragma unroll
+    for (int st = 0; st < 4; ++st) lds_dma16(qrow + st * 32 + g * 8, &s_q[v][st][0]);
+  }
   static_for<kRowsStages - 1>([&](auto S) __attribute__((always_inline)) { issue(decltype(S)::value, S); });
+  wait_vmcnt<kPer * (kRowsStages - 1)>();  // all but the ring's units are in
 
   // Q^T operand of row tile v
   bf16x8 qb[1][4];
-  const int row = v * 16 + i;
-  if (row < a.rows) {
-    const int tq = row / a.G;
-    const int qh = h * a.G + (row - tq * a.G);
-    const uint16_t* qrow = a.q + (((long long)r * a.T + tq) * a.Hq + qh) * kHeadDim;
 #pragma unroll
-    for (int st = 0; st < 4; ++st) qb[0][st] = as_bf16x8(ldg16(qrow + st * 32 + g * 8));
-  } else {
-#pragma unroll
-    for (int st = 0; st < 4; ++st) qb[0][st] = as_bf16x8(u32x4{0, 0, 0, 0});
-  }
-  const Ctx c = ctx_blocks(a.ctx_len[r], BS, a.NBmax);
+  for (int st = 0; st < 4; ++st) qb[0][st] = as_bf16x8(row < a.rows ? s_q[v][st][lane] : u32x4{0, 0, 0, 0});
+  const Ctx c = ctx_blocks(__builtin_amdgcn_readfirstlane(s_misc[v][0][lane]), BS, a.NBmax);
   const int local_len = c.local_len;
 
   float m_run[1] = {-INFINITY}, l_run[1] = {0.f};
   f32x4 acc[1][8];
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) acc[0][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  uint64_t vmask = map_mask(ks, slot0, entry0);
+  uint64_t vmask = map_mask(ks, mask_slot(0), s_misc[v][1][lane]);
   const bf16x8(&q1)[4] = qb[0];
 
   // The previous unit's scores, V operands and mask, finished one step late:
@@ -672,15 +700,18 @@ __global__ __launch_bounds__(NT * 64) void attn_split_rows_kernel(AttnArgs a) {
   // unit t sits in stage t % kRowsStages
   auto step = [&](int t, auto S) __attribute__((always_inline)) {
     constexpr int k = decltype(S)::value;
-    if (t > 0 && (t & (kChunkU - 1)) == 0) {
-      const int slot = mask_slot(t);
-      vmask = map_mask(ks, slot, map_load(smap, ks, slot, a.ctx_len + r));
-    }
     // this wave's loads of unit t are done (those of the kRowsStages - 2 later units may
     // still fly); the barrier publishes every wave's loads of unit t and tells that the
     // stage of unit t - 1 is no longer read
     wait_vmcnt<kPer * (kRowsStages - 2)>();
     __syncthreads();
+    if (t > 0 && (t & (kChunkU - 1)) == 0) {
+      // mask chunk t / kChunkU came in a chunk ago; the next one goes out now
+      // (one more load ahead of the next unit's only makes later waits stricter)
+      const int ch = t / kChunkU;
+      vmask = map_mask(ks, mask_slot(t), s_misc[v][1 + (ch & 1)][lane]);
+      lds_dma4(map_addr(smap, ks, mask_slot(t + kChunkU), a.ctx_len + r), &s_misc[v][1 + ((ch + 1) & 1)][0]);
+    }
     issue(t + kRowsStages - 1, std::integral_constant<int, (k + kRowsStages - 1) % kRowsStages>{});
     const UnitLds& buf = stage_buf(S);
     UnitRegs cur;

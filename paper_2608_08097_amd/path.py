@@ -20,7 +20,8 @@ from . import _lib as L
 class LayerState:
     """HBM state of one layer: compressed keys, scores, selection, slot map, pools."""
 
-    def __init__(self, d: L.OasisDims, num_q_tokens: int, k: int, device: str | torch.device = "cuda"):
+    def __init__(self, d: L.OasisDims, num_q_tokens: int, k: int, device: str | torch.device = "cuda",
+                 ws_attn: torch.Tensor | None = None):
         R, Hq, Hkv, D, B, NB = (d.num_reqs, d.num_q_heads, d.num_kv_heads, d.head_dim, d.block_size,
                                d.max_blocks)
         self.dims, self.T, self.k = d, int(num_q_tokens), int(k)
@@ -39,8 +40,15 @@ class LayerState:
         self.moved = torch.zeros((R, Hkv), dtype=i32, device=dev)
         self.out = torch.empty((R, self.T, Hq, D), dtype=bf, device=dev)
         self.lse = torch.empty((R, self.T, Hq), dtype=torch.float32, device=dev)
-        self.ws_attn = torch.zeros(max(1, L.oasis_attn_workspace_bytes(d, self.T, k)), dtype=torch.uint8,
-                                   device=dev)
+        # the attention's split partials: scratch of one call, so layers whose attention
+        # runs in order on one stream can share it (ws_attn, at least
+        # oasis_attn_workspace_bytes long)
+        need = max(1, L.oasis_attn_workspace_bytes(d, self.T, k))
+        if ws_attn is None:
+            ws_attn = torch.zeros(need, dtype=torch.uint8, device=dev)
+        elif ws_attn.numel() * ws_attn.element_size() < need:
+            raise ValueError(f"ws_attn holds {ws_attn.numel() * ws_attn.element_size()} bytes, {need} needed")
+        self.ws_attn = ws_attn
         self.ev_staged = None   # recorded after the last stage of this layer
         self.ev_attended = None  # recorded after the last attention of this layer
         self.layer_id = None    # id in the native issuer of the DecodePath that runs it
@@ -122,7 +130,9 @@ class DecodePath:
 
     ``host_k``/``host_v`` are the pinned host tier (bf16 pages
     ``[NPhys][Hkv][B][d]``), ``block_table`` the device page table
-    ``[R][NBmax]``.
+    ``[R][NBmax]``. The layers from ``new_layer`` share one attention
+    workspace, so their attention calls must run in order (the schedules
+    below issue them all on the caller's current stream).
     """
 
     def __init__(self, d: L.OasisDims, num_q_tokens: int, k: int, host_k: torch.Tensor, host_v: torch.Tensor,
@@ -157,9 +167,17 @@ class DecodePath:
         self.side, self.xfer = streams if streams is not None else (torch.cuda.Stream(), torch.cuda.Stream())
         # pages a growing step refreshes the local block from (None: the host tier)
         self.local_source = None
+        self._ws_attn = None  # the attention workspace of every layer (new_layer)
 
     def new_layer(self) -> LayerState:
-        return LayerState(self.dims, self.T, self.k, self.block_table.device)
+        # One attention workspace for all layers of the path: it is scratch of a
+        # single call, their attention calls run in order on the foreground stream,
+        # and a workspace that every call reuses can stay in the caches (8 x 9.4 MB
+        # fewer at 16 x 65,536 tokens and 72 rows over eight layers).
+        if self._ws_attn is None:
+            self._ws_attn = torch.zeros(max(1, L.oasis_attn_workspace_bytes(self.dims, self.T, self.k)),
+                                        dtype=torch.uint8, device=self.block_table.device)
+        return LayerState(self.dims, self.T, self.k, self.block_table.device, ws_attn=self._ws_attn)
 
     def _native_layer(self, st: LayerState) -> int:
         """Handle of the native issuer and the layer id of ``st`` (registered on first use)."""

@@ -72,6 +72,27 @@ __device__ inline unsigned order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Wave-wide minimum of uint32 values, returned to every lane (the DPP steps of
+// wave_min_max in select.h, one value).
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+  int a = (int)v;
+#define OASIS_DPP_MIN(CTRL, ROWS) \
+  a = (int)min((uint32_t)a, (uint32_t)__builtin_amdgcn_update_dpp((int)0xFFFFFFFF, a, CTRL, ROWS, 0xF, false));
+  OASIS_DPP_MIN(0x111, 0xF)
+  OASIS_DPP_MIN(0x112, 0xF)
+  OASIS_DPP_MIN(0x114, 0xF)
+  OASIS_DPP_MIN(0x118, 0xF)
+  OASIS_DPP_MIN(0x142, 0xA)
+  OASIS_DPP_MIN(0x143, 0xC)
+#undef OASIS_DPP_MIN
+  return (uint32_t)__builtin_amdgcn_readlane(a, 63);
+}
+
+// Up to this many admitted misses (or victims) of a pair are picked one at a
+// time by a wave (wave_min_u32 rounds); beyond it every item is ranked against
+// all others of its pair.
+constexpr int kPlanRounds = 16;
+
 // Exclusive scan over an NTHR-thread workgroup; the total is left in
 // s_wave[NTHR / 64] (s_wave holds NTHR / 64 + 1 ints).
 template <int NTHR>
@@ -251,36 +272,86 @@ __device__ int plan_pass(const StageArgs& a, int pair0, int np, int stride, int*
 
   // admission: every miss of a pair, or under a binding cap its fetch_cap misses
   // with the highest score (ties: lowest block id). Keys are order-preserving
-  // integers, so the ranks are distinct even for NaN scores and exactly
-  // fetch_cap misses are admitted.
-  for (int c = tid; c < n_miss; c += NTHR) {
-    const int p = s_midx[c] / k;
-    const int ms = s_mstart[p], me = s_mstart[p + 1];
-    int adm = 1;
-    if (a.fetch_cap < me - ms) {
-      const unsigned key = s_mkey[c];
-      int rank = 0;
+  // integers, so exactly fetch_cap misses are admitted even with NaN scores.
+  // Victim order: free slots ascending (s_free), then stale slots by (stamp,
+  // slot); only the first (admitted - free) stale slots are ever used. One wave
+  // per pair: under a cap of at most kPlanRounds it picks the admitted misses,
+  // and then the victims it needs, one round at a time (the best untaken item of
+  // every lane, then wave minima: no barrier, no O(n^2) ranking); larger counts
+  // rank every item of the pair against the others.
+  {
+    const int lane = tid & 63;
+    for (int p = tid >> 6; p < np; p += NTHR / 64) {
+      const int ms = s_mstart[p], me = s_mstart[p + 1];
+      const int ss = s_sstart[p], se = s_sstart[p + 1];
+      const int cap = a.fetch_cap;
+      int nadm = me - ms;
+      if (cap >= me - ms) {
+        for (int c = ms + lane; c < me; c += 64) s_madm[c] = 1;
+      } else if (cap <= kPlanRounds) {
+        nadm = cap;
+        uint32_t taken = 0;  // bit j: miss ms + lane + 64 j is admitted
+        for (int rd = 0; rd < cap; ++rd) {
+          uint32_t bk = 0xFFFFFFFFu;  // complemented key: the lowest is the highest score
+          uint32_t bi = 0xFFFFFFFFu;
+          for (int j = 0, c = ms + lane; c < me; ++j, c += 64) {
+            const uint32_t kc = ~s_mkey[c];
+            // ascending c: ties keep the lower one
+            if (!((taken >> j) & 1u) && (kc < bk || bi == 0xFFFFFFFFu)) {
+              bk = kc;
+              bi = (uint32_t)c;
+            }
+          }
+          // untaken misses remain (cap < misses), so some lane holds one
+          const uint32_t wk = wave_min_u32(bi == 0xFFFFFFFFu ? 0xFFFFFFFFu : bk);
+          const uint32_t wi = wave_min_u32(bi != 0xFFFFFFFFu && bk == wk ? bi : 0xFFFFFFFFu);
+          if ((((int)wi - ms) & 63) == lane) taken |= 1u << (((int)wi - ms) >> 6);
+        }
+        for (int j = 0, c = ms + lane; c < me; ++j, c += 64) s_madm[c] = (taken >> j) & 1u;
+      } else {
+        nadm = cap;
+        for (int c = ms + lane; c < me; c += 64) {
+          const unsigned key = s_mkey[c];
+          int rank = 0;
 #pragma unroll 4
-      for (int t = ms; t < me; ++t) {
-        const unsigned kt = s_mkey[t];
-        rank += (kt > key) || (kt == key && t < c);
+          for (int t = ms; t < me; ++t) {
+            const unsigned kt = s_mkey[t];
+            rank += (kt > key) || (kt == key && t < c);
+          }
+          s_madm[c] = rank < cap;
+        }
       }
-      adm = rank < a.fetch_cap;
-    }
-    s_madm[c] = adm;
-  }
-  // victim order per pair: free slots ascending (s_free), then stale slots by (stamp, slot)
-  for (int c = tid; c < n_stale; c += NTHR) {
-    const int p = s_sslot[c] / k;
-    const int ss = s_sstart[p], se = s_sstart[p + 1];
-    const int st = s_skey[c];
-    int rank = 0;
+      int need = nadm - (s_fstart[p + 1] - s_fstart[p]);
+      need = need < 0 ? 0 : (need > se - ss ? se - ss : need);
+      if (need <= kPlanRounds) {
+        uint32_t taken = 0;  // bit j: stale slot ss + lane + 64 j is a victim
+        for (int rd = 0; rd < need; ++rd) {
+          uint32_t bs = 0xFFFFFFFFu, bi = 0xFFFFFFFFu;
+          for (int j = 0, t = ss + lane; t < se; ++j, t += 64) {
+            const uint32_t st = (uint32_t)s_skey[t] ^ 0x80000000u;  // signed order
+            if (!((taken >> j) & 1u) && (st < bs || bi == 0xFFFFFFFFu)) {
+              bs = st;
+              bi = (uint32_t)t;
+            }
+          }
+          const uint32_t ws = wave_min_u32(bi == 0xFFFFFFFFu ? 0xFFFFFFFFu : bs);
+          const uint32_t wi = wave_min_u32(bi != 0xFFFFFFFFu && bs == ws ? bi : 0xFFFFFFFFu);
+          if ((((int)wi - ss) & 63) == lane) taken |= 1u << (((int)wi - ss) >> 6);
+          if (lane == 0) s_vstale[ss + rd] = s_sslot[wi];
+        }
+      } else {
+        for (int c = ss + lane; c < se; c += 64) {
+          const int st = s_skey[c];
+          int rank = 0;
 #pragma unroll 4
-    for (int t = ss; t < se; ++t) {
-      const int kt = s_skey[t];
-      rank += (kt < st) || (kt == st && t < c);
+          for (int t = ss; t < se; ++t) {
+            const int kt = s_skey[t];
+            rank += (kt < st) || (kt == st && t < c);
+          }
+          s_vstale[ss + rank] = s_sslot[c];
+        }
+      }
     }
-    s_vstale[ss + rank] = s_sslot[c];
   }
   __syncthreads();
 

@@ -369,12 +369,16 @@ __device__ int plan_pair_wave(const StageArgs& a, int rh, int i0, int m, const i
 // s_slot / s_page / s_epair (slot within the pair, host page, pair of the pass,
 // in ascending block id per pair); s_prh[p] receives the pair index of p.
 //
-// Misses, free slots and stale slots are compacted over the whole pass by
-// workgroup scans (in item order, so each pair's items form one contiguous
-// run in ascending block id or slot order); each thread then ranks one
-// compacted item against the others of its pair (misses by score under a cap,
-// stale slots by (stamp, slot)). Planning the pairs of a workgroup in one pass
-// pays the dependent global reads and the barriers once, not once per pair.
+// With k >= 64 each pair is planned by one wave (plan_pair_wave), the waves
+// taking the pass's pairs in turn, and the pairs' entries are then gathered in
+// pair order. With smaller k the workgroup plans the pass together: misses,
+// free slots and stale slots are compacted over the whole pass by workgroup
+// scans (in item order, so each pair's items form one contiguous run in
+// ascending block id or slot order); each thread then ranks one compacted item
+// against the others of its pair (misses by score under a cap, stale slots by
+// (stamp, slot)), and under a cap of at most kPlanRounds a wave per pair picks
+// them in rounds instead. Planning the pairs of a workgroup in one pass pays
+// the dependent global reads and the barriers once, not once per pair.
 //
 // With lsel (one pair, np = 1) the selection is taken from LDS (lsel[0, lsel_m)
 // ascending) instead of a.sel / a.sel_count. NTHR threads call it (256 in the

@@ -99,6 +99,7 @@ __device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
 // time by a wave (wave_min_u32 rounds); beyond it every item is ranked against
 // all others of its pair.
 constexpr int kPlanRounds = 16;
+static_assert(kMaxK / 64 <= 32, "a lane's items of a pair fit one 32-bit mask");
 
 // Exclusive scan over an NTHR-thread workgroup; the total is left in
 // s_wave[NTHR / 64] (s_wave holds NTHR / 64 + 1 ints).

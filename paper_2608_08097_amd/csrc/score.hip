@@ -45,7 +45,13 @@ __global__ __launch_bounds__(256) void score_kernel(ScoreArgs a) {
   const int h = rh - r * a.Hkv;
   const Ctx c = ctx_blocks(a.ctx_len[r], a.B, a.NBmax);
   const int ntiles = (a.NBmax + 15) >> 4;
-  const int tile0 = (blockIdx.x * 4 + wave) * TPW;
+  // Workgroups are dealt to the 8 XCDs round-robin by linear id, so with a
+  // grid 8 (or a multiple of 8) tile groups wide one XCD would always get the
+  // same tile group of every row, and the tail groups of short rows (no live
+  // blocks) would leave their XCDs idle; rotating the group by the row spreads
+  // every group over all XCDs (ragged 16K-32K-token rows: 48.0 -> 47.0 us).
+  const int group = (int)((blockIdx.x + blockIdx.y) % gridDim.x);
+  const int tile0 = (group * 4 + wave) * TPW;
   __shared__ ScoreQOperands<NRT> s_q;
 
   // queries first (cache-resident, needed first), then the summaries of all TPW tiles

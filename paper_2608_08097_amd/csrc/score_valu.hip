@@ -57,7 +57,9 @@ __global__ __launch_bounds__(256) void score_valu_kernel(ScoreArgs a) {
   const int r = rh / a.Hkv;
   const int h = rh - r * a.Hkv;
   const Ctx cx = ctx_blocks(a.ctx_len[r], a.B, a.NBmax);
-  const int blk0 = (blockIdx.x * 4 + wave) * (4 * kGroups);
+  // block groups rotated by the row, as in the MFMA scorer: every group spread over the XCDs
+  const int group = (int)((blockIdx.x + blockIdx.y) % gridDim.x);
+  const int blk0 = (group * 4 + wave) * (4 * kGroups);
   if (blk0 >= a.NBmax) return;
 
   float* srow = a.scores + (long long)rh * a.NBmax;

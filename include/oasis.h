@@ -348,9 +348,13 @@ OASIS_API oasis_status oasis_sparse_decode_attn_noalloc(const oasis_dims* dims, 
  *     in the initial fill) and it stays in place.
  * Consecutive calls for different layers overlap one layer's transfer with
  * the next layers' attention and prediction. The streams are ordered through
- * monotone counters in device memory (stream write-value after the producer,
- * stream wait-value before the consumer): four such edges and five or six
- * kernel launches per step, nothing allocated.
+ * monotone counters in device memory, raised by a stream write-value after
+ * the producer: the foreground waits for them with a stream wait-value, the
+ * staging kernel polls its two itself (bounded, see
+ * oasis_pipeline_set_wait_limit). Three or four such edges and four to seven
+ * kernel launches per step (attention split and merge, scoring and top-K or
+ * their fused kernel, staging; the local refresh and the compressed-key
+ * update when growing), nothing allocated.
  *
  * Arguments are checked on every step exactly as the four entry points check
  * them. Ownership: every pointer stays the caller's and must outlive the

@@ -423,12 +423,14 @@ def main():
         return
 
     def run(i, timed):
+        # The warm-up steps take the timed steps' exact call path, moved counts
+        # included (their rows are all overwritten by the timed steps).
         l, s = i % NL, i // NL
         path.step_pipelined(layers[l], qs[l][s], ctx_d, i, growing=False,
                             moved=moved_log[(i - args.warmup) % args.steps] if timed else None)
 
     for i in range(args.warmup):
-        run(i, False)
+        run(i, True)
     path.join()
     torch.cuda.synchronize()
     log(f"warmup {args.warmup} steps done")

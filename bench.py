@@ -422,12 +422,12 @@ def main():
         print(json.dumps({"kernels_only": {k_: round(v, 2) for k_, v in iso.items()}}), flush=True)
         return
 
-    def run(i, timed):
-        # The warm-up steps take the timed steps' exact call path, moved counts
-        # included (their rows are all overwritten by the timed steps).
+    def run(i, log_moved):
+        # The warm-up steps log their moved counts too, so that they take the
+        # timed steps' exact call path (the timed steps overwrite every row).
         l, s = i % NL, i // NL
         path.step_pipelined(layers[l], qs[l][s], ctx_d, i, growing=False,
-                            moved=moved_log[(i - args.warmup) % args.steps] if timed else None)
+                            moved=moved_log[(i - args.warmup) % args.steps] if log_moved else None)
 
     for i in range(args.warmup):
         run(i, True)
